@@ -1,0 +1,98 @@
+"""Test-side helpers: independent reference computations used to pin the oracle.
+
+Nothing here is imported by the decoder package.  The fold below re-scores a
+single given alignment; the exhaustive search over all alignments is a
+different method from beam search, so agreement is a real pin.
+"""
+from __future__ import annotations
+
+import itertools
+
+import numpy as np
+
+F32 = np.float32
+NEG_INF = F32(-np.inf)
+
+
+def collapse(align, V):
+    """CTC collapse of a frame-label sequence: merge repeats, drop blanks (= V)."""
+    out = []
+    prev = V
+    for c in align:
+        c = int(c)
+        if c != V and c != prev:
+            out.append(c)
+        prev = c
+    return out
+
+
+def fold_alignment(D, align, V, alpha=0.0, beta=0.0, boost_w=0.0, lm=None, bt=None):
+    """fp32 score of one alignment: the per-frame left fold of the candidate
+    score (Alg. 1 score update, Eq. 1), then LM.Final.  D: [T, V+1] fp32."""
+    s = F32(0.0)
+    last = V
+    y = []
+    q = []
+    for t, c in enumerate(align):
+        c = int(c)
+        x = F32(s + F32(D[t, c]))
+        emit = c != V and c != last
+        if emit:
+            x = F32(x + F32(beta))
+            if lm is not None:
+                x = F32(x + F32(F32(alpha) * F32(lm.score(y, c))))
+            if bt is not None:
+                sc, q2 = bt.step(q, c)
+                x = F32(x + F32(F32(boost_w) * F32(sc)))
+                q = q2
+            y.append(c)
+        last = c
+        s = x
+    if lm is not None:
+        s = F32(s + F32(F32(alpha) * F32(lm.score(y, V))))
+    return s, y
+
+
+def brute_force(D, V, **kw):
+    """Max over all (V+1)^T alignments of fold_alignment.  Returns
+    (best score, set of transcripts attaining it)."""
+    T = D.shape[0]
+    best = NEG_INF
+    arg = set()
+    for align in itertools.product(range(V + 1), repeat=T):
+        s, y = fold_alignment(D, align, V, **kw)
+        if s > best:
+            best = s
+            arg = {tuple(y)}
+        elif s == best:
+            arg.add(tuple(y))
+    return best, arg
+
+
+def greedy(D, L, V):
+    """Greedy CTC: per-frame argmax (lowest index on ties), collapse; score is
+    the fp32 left fold of the per-frame maxima."""
+    s = F32(0.0)
+    align = []
+    for t in range(L):
+        c = int(np.argmax(D[t]))
+        s = F32(s + F32(D[t, c]))
+        align.append(c)
+    return collapse(align, V), s
+
+
+def transcripts_from_trace(bp_index, W, t, K):
+    """Collapsed transcript and last label of every slot after frame t,
+    rebuilt by walking the backpointers."""
+    V = W - 1
+    res = []
+    for j in range(K):
+        labels = []
+        jj = j
+        for tt in range(t, -1, -1):
+            i = int(bp_index[tt, jj])
+            labels.append(i % W)
+            jj = i // W
+        labels.reverse()
+        res.append((tuple(collapse(labels, V)), labels[-1]))
+    return res
