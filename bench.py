@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""Benchmark of the batched CTC beam-search step on one MI355X.
+
+One *step* is one ``ctcbeam_decode`` launch: every frame of every utterance of
+the workload (Algorithm 1 from initialisation to LM.Final, plus read-out).
+Default workload: B=64 utterances, T=400 padded frames, V=1024 BPE tokens +
+blank, beam K=8, 3-gram backoff LM (1024 unigrams, 300k bigrams, 1M trigrams),
+alpha=0.5, beta=1.0 - synthetic, seeded, shaped like the paper's setting.
+
+Prints ONE JSON line:
+  value      = B*T / (mean launch time)   [decoded frames/s, padded frames]
+  roofline   = algorithmic bytes per launch / mean launch time vs 8 TB/s HBM;
+               the bytes come from the kernel's own counters (an untimed
+               launch with statistics on): per utterance-frame 4*(V+1) for the
+               log-prob row + 4*K back-pointers, per live beam-frame 12 B per
+               LM/boosting chain state + 6 B per explicit continuation scanned,
+               4 B per emitting winner; per utterance 8*V staging + 4*T + 4
+               output bytes.
+  cpu_baseline = the CPU oracle timed on a bounded sample of the same
+               workload (a reported baseline, not a target).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "decoded frames/sec (B×T/s) at K=8, V=1024 + 3-gram LM; % HBM roofline"
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in ("ctcbeam_kernel.hip", "ctcbeam_internal.h"):
+        with open(os.path.join(ROOT, "paper_2508_07315_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(stats, B: int, T: int, V: int, K: int) -> int:
+    """Bytes the method must move for one launch (see module docstring)."""
+    W = V + 1
+    s = stats.astype("int64")
+    frames = int(s[:, 0].sum())
+    per_frame = frames * (4 * W + 4 * K)
+    chains = 12 * int(s[:, 2].sum()) + 6 * int(s[:, 3].sum()) + 12 * int(s[:, 4].sum()) + \
+        6 * int(s[:, 5].sum())
+    emit = 4 * int(s[:, 6].sum())
+    per_utt = B * (8 * V + 4 * T + 4)
+    return per_frame + chains + emit + per_utt
+
+
+def load_traffic(workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_sha") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, lp, lens, n_utts: int, threads: int):
+    import numpy as np
+
+    import oracle
+    import workloads as W
+    idx = list(range(min(n_utts, w.B)))
+    lm = oracle.LM(W.lm_for(w.lm, w.V)) if w.lm is not None else None
+    bt = None
+    if w.boost is not None:
+        off, tok = W.phrases_for(w.boost, w.V)
+        bt = oracle.BT(w.V, off, tok)
+    t0 = time.perf_counter()
+    oracle.decode(lp[idx], lens[idx], w.K, w.alpha, w.beta, w.boost_w, theta=w.theta, lm=lm, bt=bt,
+                  n_threads=threads)
+    dt = time.perf_counter() - t0
+    frames = len(idx) * w.T
+    return dict(value=frames / dt, unit="frames/s", cores=min(threads, len(idx)), kind="oracle",
+                sample=f"{len(idx)} of {w.B} utterances ({int(np.sum(lens[idx]))} valid frames, "
+                       f"T={w.T} padded) of the same workload, {dt:.2f} s wall",
+                valid_frames_per_s=float(np.sum(lens[idx])) / dt)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3, help="workload 1..5 (default 3)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-utts", type=int, default=8)
+    ap.add_argument("--cpu-threads", type=int, default=8)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the "
+              "decoder shards utterances across GPUs only in design, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2508_07315_amd as P
+    import workloads as W
+
+    P._load()  # no CPU fallback: fails loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    w = W.CONFIGS[args.config]
+    t_setup = time.perf_counter()
+    lens = W.make_lengths(w)
+    lp = W.make_logprobs(w)
+    lm = P.ctcbeam_lm_build(W.lm_for(w.lm, w.V)) if w.lm is not None else None
+    bt = None
+    if w.boost is not None:
+        off, tok = W.phrases_for(w.boost, w.V)
+        bt = P.ctcbeam_boost_build(w.V, off, tok)
+    d_lp = torch.from_numpy(lp).to(dev)
+    d_len = torch.from_numpy(lens).to(dev)
+    B, T, V, K = w.B, w.T, w.V, w.K
+    out_tok = torch.empty((B, T), dtype=torch.int32, device=dev)
+    out_len = torch.empty((B,), dtype=torch.int32, device=dev)
+    out_sc = torch.empty((B,), dtype=torch.float32, device=dev)
+    ws = torch.empty((P.ctcbeam_workspace_bytes(B, T, K),), dtype=torch.uint8, device=dev)
+    stats = torch.zeros((B, 8), dtype=torch.int64, device=dev)
+    print(f"# setup {time.perf_counter() - t_setup:.1f} s: {w.name}", file=sys.stderr, flush=True)
+
+    def launch(st=None):
+        P.ctcbeam_decode_ex(d_lp, d_len, K, w.alpha, w.beta, w.boost_w, lm, bt, ws, out_tok,
+                            out_len, out_sc, theta=w.theta, stats=st)
+
+    # untimed launch with the kernel's counters on: algorithmic bytes
+    launch(stats)
+    torch.cuda.synchronize()
+    alg_bytes = algorithmic_bytes(stats.cpu().numpy(), B, T, V, K)
+    status = P.ctcbeam_query_status(ws, B)
+    for _ in range(args.warmup):
+        launch()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for e0, e1 in ev:
+        e0.record(stream)
+        launch()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    k_ms = [e0.elapsed_time(e1) for e0, e1 in ev]
+    mean_ms = float(np.mean(k_ms))
+    ms_per_step = wall * 1e3 / args.steps
+    value = B * T / (mean_ms * 1e-3)
+    achieved = alg_bytes / (mean_ms * 1e-3) / 1e9
+    traffic = load_traffic(w.name)
+    result = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "T": T, "V": V, "K": K,
+                   "lm": None if w.lm is None else f"{w.lm.order}-gram, {'/'.join(str(c) for c in w.lm.counts)} explicit n-grams",
+                   "boost": None if w.boost is None else f"{w.boost.n_phrases} phrases",
+                   "alpha": w.alpha, "beta": w.beta, "boost_w": w.boost_w, "theta": w.theta,
+                   "parallelism": "one workgroup per utterance"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic},
+        "kernel_ms_mean": mean_ms,
+        "kernel_ms_min": float(np.min(k_ms)),
+        "algorithmic_bytes_per_launch": alg_bytes,
+        "valid_frames_per_s": float(np.sum(lens)) / (mean_ms * 1e-3),
+        "us_per_frame_step": mean_ms * 1e3 / T,
+        "status_bits": status,
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, lp, lens, args.cpu_utts,
+                                              max(1, min(args.cpu_threads, os.cpu_count() or 1)))
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,72 @@
+// Internal layouts shared by the host builders and the gfx950 kernel.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ctcbeam {
+
+constexpr int kThreads = 512;         // threads per workgroup (8 wave64)
+constexpr int kWaves = kThreads / 64;
+constexpr int kMaxK = 64;             // beam size limit
+constexpr int kMaxLev = 7;            // LM order - 1 limit
+constexpr int kKeyWords = 8192;       // per-chunk [hyp][token] key rows (u32 each)
+constexpr int kLmStage = 4096;        // staged LM arcs per chunk
+constexpr int kBtStage = 2048;        // staged boosting continuations per chunk
+constexpr int kCap = 512;             // candidate buffer entries
+constexpr uint32_t kExists = 0x80000000u;
+
+// LM state record, one per chain level l (context of length l+1):
+//   {arc_begin, arc_count | kExists, backoff bits}
+struct LmLevel {
+  uint32_t begin;
+  uint32_t count;   // low 31 bits: arcs; bit 31: the context is an entry
+  float bo;
+};
+// LM arc: ln probability of (context, token), next state after emitting token
+struct LmArc {
+  float logp;
+  uint32_t target;
+  uint32_t token;
+};
+// Boosting tree state record.
+struct BtNode {
+  uint32_t list_begin;
+  uint32_t list_count;
+  uint32_t pot;        // low 8 bits: pot; bits 8..31: chain nodes (statistics)
+  uint32_t chain_arcs; // statistics only
+};
+struct BtEntry {
+  uint32_t token;
+  uint32_t key;        // (prio << 26) | (pre << 20) | child
+};
+constexpr uint32_t kBtChildMask = (1u << 20) - 1;
+
+struct KernelParams {
+  const float* logprobs;
+  const int32_t* lengths;
+  int B, T, V, K;
+  float alpha, beta, boost_w, theta;
+  // LM (null when disabled)
+  const LmLevel* lm_states;
+  const LmArc* lm_arcs;
+  const float* lm_unigram;   // [V+1], index V = </s>
+  int lm_nlev;
+  uint32_t lm_bos_state;
+  // boosting (null when disabled)
+  const BtNode* bt_nodes;
+  const BtEntry* bt_list;
+  const uint32_t* bt_root_key;  // [V]
+  // workspace / outputs
+  uint32_t* status;          // [B]
+  int32_t* bp;               // [B, T, K]
+  int32_t* out_tokens;       // [B, T]
+  int32_t* out_lengths;      // [B] or null
+  float* out_scores;         // [B]
+  int64_t* stats;            // [B, 8] or null
+};
+
+// Enqueue the decode kernel; returns a hipError_t.
+hipError_t launch_decode(const KernelParams& p, hipStream_t stream);
+
+}  // namespace ctcbeam

@@ -194,69 +194,99 @@ def _encode(ids: np.ndarray, base: int) -> np.ndarray:
     return code
 
 
+def _race_topk(rng, ctxs, group_start, group_len, items, weights, counts, chunk=8_000_000):
+    """Exponential-race (Efraimidis-Spirakis) selection: for each context in
+    ctxs (ascending) keep the counts[ctx] admissible items with the largest
+    log(u)/weight keys.  Processed in chunks of contexts to bound memory."""
+    out_c, out_i = [], []
+    lens_all = group_len[ctxs]
+    bounds = [0]
+    acc = 0
+    for j, n in enumerate(lens_all.tolist()):
+        acc += n
+        if acc >= chunk:
+            bounds.append(j + 1)
+            acc = 0
+    if bounds[-1] != len(ctxs):
+        bounds.append(len(ctxs))
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        cs = ctxs[a:b]
+        lens = group_len[cs]
+        tot = int(lens.sum())
+        if tot == 0:
+            continue
+        seg0 = np.repeat(np.cumsum(lens) - lens, lens)
+        ctx_rep = np.repeat(cs, lens)
+        within = np.arange(tot) - seg0
+        it = items[np.repeat(group_start[cs], lens) + within]
+        key = np.log(rng.random(tot)) / weights[it]
+        order = np.lexsort((-key, ctx_rep))
+        rank = within  # ctx_rep is already grouped in ascending context order
+        keep = rank < np.repeat(counts[cs], lens)
+        out_c.append(ctx_rep[order][keep])
+        out_i.append(it[order][keep])
+    if not out_c:
+        return np.zeros(0, np.int64), np.zeros(0, np.int64)
+    return np.concatenate(out_c), np.concatenate(out_i)
+
+
 def _sample_without_replacement(rng, n_ctx, group_start, group_len, items, weights,
-                                counts, max_rounds=40):
+                                counts, max_rounds=32):
     """For each context i pick counts[i] distinct items out of
-    items[group_start[i] : group_start[i]+group_len[i]], Zipf-weighted
-    (sequential draws proportional to weight among the items not yet taken,
-    realised as batched rejection of repeats).  Returns (ctx_of_pick, item)."""
+    items[group_start[i] : group_start[i]+group_len[i]], Zipf-weighted without
+    replacement (draws proportional to weight among the items not yet taken).
+    Contexts that take their whole admissible set take it directly; contexts
+    that take more than a quarter of it use an exponential race; the rest use
+    batched draws with rejection of repeats (the same distribution), and any
+    context still short after max_rounds is redone with the race."""
     counts = counts.astype(np.int64)
-    full = counts >= group_len
-    picks_ctx = []
-    picks_item = []
-    # contexts that take their whole admissible set
-    fi = np.nonzero(full & (counts > 0))[0]
+    picks_ctx, picks_item = [], []
+    full = (counts >= group_len) & (counts > 0)
+    fi = np.nonzero(full)[0]
     if len(fi):
         lens = group_len[fi]
         ctx = np.repeat(fi, lens)
-        starts = np.repeat(group_start[fi], lens)
         within = np.arange(len(ctx)) - np.repeat(np.cumsum(lens) - lens, lens)
         picks_ctx.append(ctx)
-        picks_item.append(items[starts + within])
-    todo = np.nonzero(~full & (counts > 0))[0]
-    if len(todo) == 0:
-        return np.concatenate(picks_ctx) if picks_ctx else np.zeros(0, np.int64), \
-            np.concatenate(picks_item) if picks_item else np.zeros(0, np.int64)
-    cw = np.concatenate([[0.0], np.cumsum(weights[items].astype(np.float64))])
-    n_items_code = int(items.max()) + 1 if len(items) else 1
-    acc_codes = np.zeros(0, dtype=np.int64)
-    got = np.zeros(n_ctx, dtype=np.int64)
-    for _ in range(max_rounds):
-        need = counts[todo] - got[todo]
-        sel = need > 0
-        if not sel.any():
-            break
-        ctx = np.repeat(todo[sel], need[sel])
-        g0 = group_start[ctx]
-        g1 = g0 + group_len[ctx]
-        lo = cw[g0]
-        hi = cw[g1]
-        u = lo + rng.random(len(ctx)) * (hi - lo)
-        pos = np.searchsorted(cw, u, side="right") - 1
-        pos = np.clip(pos, g0, g1 - 1)
-        item = items[pos]
-        code = ctx.astype(np.int64) * n_items_code + item
-        _, first = np.unique(code, return_index=True)
-        first.sort()
-        code = code[first]
-        fresh = ~np.isin(code, acc_codes, assume_unique=False)
-        code = code[fresh]
-        acc_codes = np.concatenate([acc_codes, code])
-        got += np.bincount((code // n_items_code).astype(np.int64), minlength=n_ctx)
-    # deterministic completion of any context still short: heaviest first
-    short = todo[(counts[todo] - got[todo]) > 0]
-    if len(short):
-        acc_sorted = np.sort(acc_codes)
-        extra = []
-        for i in short:
-            g = items[group_start[i]: group_start[i] + group_len[i]]
-            order = g[np.argsort(-weights[g], kind="stable")]
-            have = set((acc_sorted[(acc_sorted // n_items_code) == i] % n_items_code).tolist())
-            add = [x for x in order.tolist() if x not in have][: counts[i] - got[i]]
-            extra.extend(i * n_items_code + x for x in add)
-        acc_codes = np.concatenate([acc_codes, np.asarray(extra, dtype=np.int64)])
-    picks_ctx.append(acc_codes // n_items_code)
-    picks_item.append(acc_codes % n_items_code)
+        picks_item.append(items[np.repeat(group_start[fi], lens) + within])
+    dense = (~full) & (counts > 0) & (4 * counts > group_len)
+    di = np.nonzero(dense)[0]
+    if len(di):
+        c, i = _race_topk(rng, di, group_start, group_len, items, weights, counts)
+        picks_ctx.append(c)
+        picks_item.append(i)
+    todo = np.nonzero((~full) & (~dense) & (counts > 0))[0]
+    if len(todo):
+        cw = np.concatenate([[0.0], np.cumsum(weights[items].astype(np.float64))])
+        base = int(items.max()) + 1
+        acc = np.zeros(0, dtype=np.int64)
+        got = np.zeros(n_ctx, dtype=np.int64)
+        for _ in range(max_rounds):
+            need = counts[todo] - got[todo]
+            sel = need > 0
+            if not sel.any():
+                break
+            ctx = np.repeat(todo[sel], need[sel])
+            g0 = group_start[ctx]
+            g1 = g0 + group_len[ctx]
+            u = cw[g0] + rng.random(len(ctx)) * (cw[g1] - cw[g0])
+            pos = np.clip(np.searchsorted(cw, u, side="right") - 1, g0, g1 - 1)
+            code = ctx.astype(np.int64) * base + items[pos]
+            _, first = np.unique(code, return_index=True)
+            code = code[np.sort(first)]
+            code = code[~np.isin(code, acc)]
+            acc = np.concatenate([acc, code])
+            got += np.bincount(code // base, minlength=n_ctx)
+        short = todo[(counts[todo] - got[todo]) > 0]
+        if len(short):
+            acc = acc[~np.isin(acc // base, short)]
+            c, i = _race_topk(rng, short, group_start, group_len, items, weights, counts)
+            picks_ctx.append(c)
+            picks_item.append(i)
+        picks_ctx.append(acc // base)
+        picks_item.append(acc % base)
+    if not picks_ctx:
+        return np.zeros(0, np.int64), np.zeros(0, np.int64)
     return np.concatenate(picks_ctx), np.concatenate(picks_item)
 
 
