@@ -39,7 +39,7 @@ METRIC = "decoded frames/sec (B×T/s) at K=8, V=1024 + 3-gram LM; % HBM roofline
 
 def kernel_source_hash() -> str:
     h = hashlib.sha256()
-    for f in ("ctcbeam_kernel.hip", "ctcbeam_internal.h"):
+    for f in ("ctcbeam_decode.inl", "ctcbeam_internal.h"):
         with open(os.path.join(ROOT, "paper_2508_07315_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

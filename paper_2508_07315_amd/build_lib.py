@@ -30,14 +30,26 @@ def _run(cmd):
         raise RuntimeError("command failed: " + " ".join(cmd))
 
 
-def build(verbose: bool = False) -> str:
+KERNEL_UNITS = ["ctcbeam_kernel_lpt1.hip", "ctcbeam_kernel_lpt2.hip", "ctcbeam_kernel_lpt4.hip",
+                "ctcbeam_kernel_lpt8.hip"]
+
+
+def build(verbose: bool = False, jobs: int = 0) -> str:
+    from concurrent.futures import ThreadPoolExecutor
+    jobs = jobs or max(1, min(len(KERNEL_UNITS) + 1, os.cpu_count() or 1))
     with tempfile.TemporaryDirectory(prefix="ctcbeam_build_") as tmp:
-        k_o = os.path.join(tmp, "kernel.o")
+        cmds, objs = [], []
+        for unit in KERNEL_UNITS:
+            o = os.path.join(tmp, unit.replace(".hip", ".o"))
+            cmds.append(["hipcc", *COMMON, *DEVICE, "-c", os.path.join(CSRC, unit), "-o", o])
+            objs.append(o)
         h_o = os.path.join(tmp, "host.o")
-        _run(["hipcc", *COMMON, *DEVICE, "-c", os.path.join(CSRC, "ctcbeam_kernel.hip"), "-o", k_o])
-        _run(["hipcc", *COMMON, "-c", os.path.join(CSRC, "ctcbeam_host.cpp"), "-o", h_o])
+        cmds.append(["hipcc", *COMMON, "-c", os.path.join(CSRC, "ctcbeam_host.cpp"), "-o", h_o])
+        objs.append(h_o)
+        with ThreadPoolExecutor(jobs) as ex:
+            list(ex.map(_run, cmds))
         out_tmp = LIB + f".tmp{os.getpid()}"
-        _run(["hipcc", *DEVICE, "-shared", "-fPIC", k_o, h_o, "-o", out_tmp])
+        _run(["hipcc", *DEVICE, "-shared", "-fPIC", *objs, "-o", out_tmp])
         os.replace(out_tmp, LIB)
     if verbose:
         print("built", LIB)

@@ -231,8 +231,9 @@ int build_lm_tables(int order, int V, const int64_t* counts, const int32_t* cons
   std::vector<int64_t> arc_off(order + 2, 0);
   for (int m = 2; m <= order; ++m) arc_off[m + 1] = arc_off[m] + ord[m].n;
   const int64_t n_arcs = arc_off[order + 1];
-  if (n_arcs >= (int64_t(1) << 32) || n_states >= (int64_t(1) << 32))
-    return fail(2, "LM too large for 32-bit indices");
+  // state ids stay below 2^31: the kernel tags staged keys with bit 31
+  if (n_arcs >= (int64_t(1) << 32) || n_states >= (int64_t(1) << 31))
+    return fail(2, "LM too large for the 31-bit state / 32-bit arc indices");
   std::vector<uint32_t> sbeg(n_states, 0), scnt(n_states, 0);
   std::vector<float> sbo(n_states, 0.0f);
   std::vector<uint8_t> sexists(n_states, 0);

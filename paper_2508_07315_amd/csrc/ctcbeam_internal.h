@@ -66,7 +66,19 @@ struct KernelParams {
   int64_t* stats;            // [B, 8] or null
 };
 
-// Enqueue the decode kernel; returns a hipError_t.
-hipError_t launch_decode(const KernelParams& p, hipStream_t stream);
+// Kernel variants by labels per lane (V <= 512 * LPT); each dispatches on the
+// LM order and on boosting.  Return the launch's hipError_t.
+hipError_t launch_lpt1(const KernelParams& p, hipStream_t stream);
+hipError_t launch_lpt2(const KernelParams& p, hipStream_t stream);
+hipError_t launch_lpt4(const KernelParams& p, hipStream_t stream);
+hipError_t launch_lpt8(const KernelParams& p, hipStream_t stream);
+
+inline hipError_t launch_decode(const KernelParams& p, hipStream_t stream) {
+  if (p.B == 0) return hipSuccess;
+  if (p.V <= 512) return launch_lpt1(p, stream);
+  if (p.V <= 1024) return launch_lpt2(p, stream);
+  if (p.V <= 2048) return launch_lpt4(p, stream);
+  return launch_lpt8(p, stream);
+}
 
 }  // namespace ctcbeam
