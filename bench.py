@@ -102,6 +102,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-utts", type=int, default=8)
     ap.add_argument("--cpu-threads", type=int, default=8)
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, run a plain device copy of this many MiB three times "
+                         "(calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE against known bytes)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the "
@@ -192,6 +195,14 @@ def main():
         "us_per_frame_step": mean_ms * 1e3 / T,
         "status_bits": status,
     }
+    if args.copy_mib > 0:
+        n = args.copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = n * 4
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, lp, lens, args.cpu_utts,
                                               max(1, min(args.cpu_threads, os.cpu_count() or 1)))
