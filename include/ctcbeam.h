@@ -115,7 +115,7 @@ void ctcbeam_lm_free(ctcbeam_lm* lm);
  *                tokens[offsets[p] .. offsets[p+1]); empty phrases are ignored
  *   tokens     : host token ids in 0..V-1
  * Limits (return 2 beyond them): at most 2^20-1 tree nodes, phrase length at
- * most 62, at most 2048 boosted continuations per tree state.
+ * most 62.
  * Ownership and synchrony as for ctcbeam_lm_build.
  */
 int ctcbeam_boost_build(int vocab_size, int n_phrases, const int32_t* offsets,

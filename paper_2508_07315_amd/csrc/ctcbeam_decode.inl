@@ -11,39 +11,45 @@
 // label).
 //
 // Design (MI355X, CDNA4): the search is a serial chain over frames, so each
-// utterance is one persistent workgroup of 8 wave64 that keeps every beam's
-// state in LDS and loops over its own frames with no host round trip.  The
-// B utterances are independent workgroups.  There is no dense contraction:
-// the work is gathers of LM arcs, VALU scoring and a selection, bound by
-// memory latency, LDS traffic and VALU issue, so MFMA is not used.
+// utterance is one persistent workgroup of 8 wave64 that loops over its own
+// frames with no host round trip; the B utterances are independent
+// workgroups.  There is no dense contraction: the work is gathers of LM arcs,
+// VALU scoring and a selection, bound by dependent latency (LDS round trips,
+// cross-lane chains, barriers), so MFMA is not used.
 //
-// Per frame (single chunk when K*V fits the LDS key rows, e.g. K=8, V=1024):
-//   1. the next frame's log-prob row is prefetched into registers (lane owns
-//      labels c = tid + j*512);
-//   2. fill: one wave per live beam gathers the explicit continuations of
-//      every state of its LM backoff chain (all loads of a beam issued before
-//      the first use, so one memory latency covers the chain) and scatters
-//      them into an LDS [beam][token] key row with atomicMax on
-//      (order << 28 | staging slot): the highest-order n-gram wins with no
-//      barrier between orders; boosting continuations (merged per tree state
-//      on the host) are stored the same way;
-//   3. candidates: each lane scores its labels for every beam in registers,
-//      resolving the LM value from the key row or from the unigram + backoff
-//      fold (compile-time LM order);
-//   4. selection: the K-th largest of 64 lane maxima (each wave sorts its
-//      lane maxima in registers, every wave then sorts the union of the waves'
-//      top 8) is a lower bound on the K-th best candidate; it filters K*V
-//      candidates down to a few dozen survivors in LDS;
-//   5. wave 0 sorts the survivors in registers (bitonic, score desc / index
-//      asc), prefetching the chain headers of every emitting survivor before
-//      the sort, then prunes, advances the beams (hash of the collapsed
-//      transcript, LM/boost states), recombines duplicates and builds the next
-//      frame's live list; the other waves clear the key rows meanwhile.
-//      Back-pointers go to HBM.
-// Large beams (K*V above the key rows) run the fill/score/filter per chunk of
-// beams with a running bound and compaction.  Rare overflows of the survivor
-// buffer fall back to an exact extraction.  After the last frame the best
-// beam is traced back through the back-pointers staged in LDS.
+// Every wave keeps the whole beam (slot j in lane j: score, last label,
+// transcript hash, LM/boosting states and their backoff chains) in registers.
+// Each wave runs the beam update itself on the same inputs, so the next
+// frame's fill starts without a hand-off between waves.  Per frame (one
+// chunk when K*V fits the LDS key rows, e.g. K=8, V=1024), with 4 barriers:
+//   F. fill: the explicit continuations of every live beam's LM backoff chain
+//      (and its merged boosting continuation list) are cut into tiles of 64
+//      and spread over all waves; each lane loads one arc per tile and
+//      scatters it into an LDS [beam][token] row: LM entries are 64-bit
+//      (generation | order | staging slot : alpha*value) combined with an
+//      atomic max, so the highest-order n-gram wins in any order; boosting
+//      entries are generation-tagged keys.  Entries of older generations read
+//      as absent, so the rows are never cleared (except when the 6-bit
+//      generation wraps).
+//   C. candidates: each lane scores its labels for every beam of the chunk in
+//      registers (beam data by readlane), resolving the LM value from the row
+//      or from the unigram + backoff fold, and publishes the maximum of each
+//      16-lane row.
+//   T. filter: the K-th largest of those disjoint-group maxima is a lower
+//      bound on the K-th best candidate; candidates at or above it (a few
+//      dozen) are appended to a survivor pool in LDS.
+//   R. rank: the pool (survivors plus K reserved entries holding the blank
+//      candidates, or the best K of earlier chunks) is ranked exactly by
+//      (score desc, flat index asc): each wave ranks an eighth of the pool
+//      against all of it with ballots, and the best K go to a reserved region
+//      in rank order.
+//   U. update: prune, advance (hash of the collapsed transcript, LM/boosting
+//      states, chain headers fetched for emitting winners), recombine, plan
+//      the next frame's chunks, write back-pointers to HBM.
+// Large beams (K*V above the key rows) repeat F/C/T/R per chunk of beams with
+// a running bound.  A survivor pool overflow falls back to an exact
+// extraction.  After the last frame the best beam is traced back through the
+// back-pointers staged in LDS.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -54,18 +60,16 @@ namespace detail {
 
 constexpr float kNegInf = -__builtin_huge_valf();
 
-// LDS scratch carved from one block so the traceback can reuse it.
-constexpr int kBigWords = 2 * kKeyWords + 3 * kLmStage + kBtStage;
-constexpr int kOffLmKey = 0;
-constexpr int kOffBtKey = kKeyWords;
-constexpr int kOffStV = 2 * kKeyWords;
-constexpr int kOffStTgt = kOffStV + kLmStage;
-constexpr int kOffStKey = kOffStTgt + kLmStage;
-constexpr int kOffBtClr = kOffStKey + kLmStage;
-// label survivors may fill the buffer up to kChunkCap; the remaining kMaxK
-// entries always take the blank candidates
-constexpr int kChunkCap = kCap - kMaxK;
-constexpr int kFillUnroll = 16;
+// LDS scratch carved from one block so the traceback can reuse it:
+// [LM rows: kKeyWords x u64][boosting rows: kKeyWords x u32][LM targets].
+constexpr int kBigWords = 3 * kKeyWords + kLmStage;
+constexpr int kOffBtRow = 2 * kKeyWords;
+constexpr int kOffTgt = 3 * kKeyWords;
+// generation tag in the top 6 bits of LM entry high words and boosting keys
+constexpr int kGenShift = 26;
+constexpr uint32_t kGenMax = 63u;
+constexpr uint32_t kLowMask = (1u << kGenShift) - 1u;
+constexpr int kTileUnroll = 8;
 
 __device__ __forceinline__ uint64_t mix_token(uint64_t h, uint32_t c) {
   uint64_t z = h + (static_cast<uint64_t>(c) + 1ull) * 0x9E3779B97F4A7C15ull;
@@ -82,18 +86,17 @@ __device__ __forceinline__ uint64_t order_key(float x, uint32_t idx) {
   return (static_cast<uint64_t>(u) << 32) | static_cast<uint64_t>(0xFFFFFFFFu - idx);
 }
 
-__device__ __forceinline__ bool beats(float xf, uint32_t if_, float xe, uint32_t ie) {
-  return (xf > xe) || (xf == xe && if_ < ie);
-}
-
 __device__ __forceinline__ uint64_t lanemask_lt() {
   const uint32_t lane = threadIdx.x & 63u;
   return lane == 0 ? 0ull : (~0ull >> (64u - lane));
 }
 
-__device__ __forceinline__ void wave_sync_lds() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
+__device__ __forceinline__ int rdlane(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ uint32_t rdlane(uint32_t v, int l) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), l));
+}
+__device__ __forceinline__ float rdlane(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
 
 // ---- cross-lane exchange on gfx950 without the LDS crossbar ----
@@ -104,6 +107,28 @@ template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_mov(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), CTRL, 0xF, 0xF, false));
 }
+// DPP move for patterns whose source lane is valid for every lane
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_full(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), CTRL, 0xF, 0xF, false));
+}
+// per-lane predicate from a compile-time lane mask (an SGPR constant used as
+// the select mask, no per-lane arithmetic)
+__device__ __forceinline__ bool lane_in(uint64_t mask) { return __builtin_amdgcn_inverse_ballot_w64(mask); }
+// the same, with the constant materialised where it is used: loops with many
+// such masks would otherwise keep them all live in SGPRs across the loop
+template <uint64_t M>
+__device__ __forceinline__ bool lane_in_here() {
+  uint32_t lo, hi;
+  asm volatile("s_mov_b32 %0, %1" : "=s"(lo) : "i"(static_cast<uint32_t>(M)));
+  asm volatile("s_mov_b32 %0, %1" : "=s"(hi) : "i"(static_cast<uint32_t>(M >> 32)));
+  return __builtin_amdgcn_inverse_ballot_w64((static_cast<uint64_t>(hi) << 32) | lo);
+}
+constexpr uint64_t kLanesBit2 = 0xF0F0F0F0F0F0F0F0ull;   // lane & 4
+constexpr uint64_t kLanesBit4 = 0xFFFF0000FFFF0000ull;   // lane & 16
+constexpr uint64_t kLanesBit5 = 0xFFFFFFFF00000000ull;   // lane & 32
+constexpr uint64_t kLanesGe16 = 0xFFFFFFFFFFFF0000ull;
+constexpr uint64_t kLanesGe48 = 0xFFFF000000000000ull;
 template <int CTRL>
 __device__ __forceinline__ float dpp_movf(float v, float old) {
   return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(old), __float_as_int(v), CTRL, 0xF, 0xF, false));
@@ -120,30 +145,28 @@ constexpr int kDppRowRor8 = 0x128;
 // value of lane (lane ^ j); j must be a compile-time power of two <= 32 after
 // unrolling
 __device__ __forceinline__ uint32_t xor_lane(uint32_t v, int j, int lane) {
+  (void)lane;
   switch (j) {
-    case 1: return dpp_mov<kDppQuadXor1>(v);
-    case 2: return dpp_mov<kDppQuadXor2>(v);
+    case 1: return dpp_full<kDppQuadXor1>(v);
+    case 2: return dpp_full<kDppQuadXor2>(v);
     case 4: {
       const uint32_t up = dpp_mov<kDppRowShl4>(v);
       const uint32_t dn = dpp_mov<kDppRowShr4>(v);
-      return (lane & 4) ? dn : up;
+      return lane_in(kLanesBit2) ? dn : up;
     }
-    case 8: return dpp_mov<kDppRowRor8>(v);
+    case 8: return dpp_full<kDppRowRor8>(v);
     case 16: {
       const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
-      return (lane & 16) ? static_cast<uint32_t>(r[0]) : static_cast<uint32_t>(r[1]);
+      return lane_in(kLanesBit4) ? static_cast<uint32_t>(r[0]) : static_cast<uint32_t>(r[1]);
     }
     default: {
       const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
-      return (lane & 32) ? static_cast<uint32_t>(r[0]) : static_cast<uint32_t>(r[1]);
+      return lane_in(kLanesBit5) ? static_cast<uint32_t>(r[0]) : static_cast<uint32_t>(r[1]);
     }
   }
 }
 __device__ __forceinline__ float xor_lane(float v, int j, int lane) {
   return __uint_as_float(xor_lane(__float_as_uint(v), j, lane));
-}
-__device__ __forceinline__ int xor_lane(int v, int j, int lane) {
-  return static_cast<int>(xor_lane(static_cast<uint32_t>(v), j, lane));
 }
 
 // inclusive prefix sum over the wave
@@ -152,45 +175,69 @@ __device__ __forceinline__ int wave_incl_scan(int v, int lane) {
   v += static_cast<int>(dpp_mov<kDppRowShr2>(static_cast<uint32_t>(v)));
   v += static_cast<int>(dpp_mov<kDppRowShr4>(static_cast<uint32_t>(v)));
   v += static_cast<int>(dpp_mov<kDppRowShr8>(static_cast<uint32_t>(v)));
+  (void)lane;
   const int r0 = __builtin_amdgcn_readlane(v, 15);
   const int r1 = __builtin_amdgcn_readlane(v, 31);
   const int r2 = __builtin_amdgcn_readlane(v, 47);
-  v += (lane >= 16 ? r0 : 0) + (lane >= 32 ? r1 : 0) + (lane >= 48 ? r2 : 0);
+  v += lane_in(kLanesGe16) ? r0 : 0;
+  v += lane_in(kLanesBit5) ? r1 : 0;
+  v += lane_in(kLanesGe48) ? r2 : 0;
   return v;
 }
 
 // maximum over each 16-lane row, valid in the row's last lane
+__device__ __forceinline__ float fmax_sel(float a, float b) { return (b > a) ? b : a; }
 __device__ __forceinline__ float row_max_last(float v) {
   const float ni = -__builtin_huge_valf();
-  v = fmaxf(v, dpp_movf<kDppRowShr1>(v, ni));
-  v = fmaxf(v, dpp_movf<kDppRowShr2>(v, ni));
-  v = fmaxf(v, dpp_movf<kDppRowShr4>(v, ni));
-  v = fmaxf(v, dpp_movf<kDppRowShr8>(v, ni));
+  v = fmax_sel(v, dpp_movf<kDppRowShr1>(v, ni));
+  v = fmax_sel(v, dpp_movf<kDppRowShr2>(v, ni));
+  v = fmax_sel(v, dpp_movf<kDppRowShr4>(v, ni));
+  v = fmax_sel(v, dpp_movf<kDppRowShr8>(v, ni));
   return v;
 }
 
 // maximum over each 8-lane group, valid in every lane of the group
 __device__ __forceinline__ float group8_max(float v, int lane) {
-  v = fmaxf(v, xor_lane(v, 1, lane));
-  v = fmaxf(v, xor_lane(v, 2, lane));
-  v = fmaxf(v, xor_lane(v, 4, lane));
+  v = fmax_sel(v, xor_lane(v, 1, lane));
+  v = fmax_sel(v, xor_lane(v, 2, lane));
+  v = fmax_sel(v, xor_lane(v, 4, lane));
   return v;
 }
 
+// lanes that keep the larger value in the bitonic step (k, j) of a sort of
+// groups of N lanes, descending
+constexpr uint64_t bitonic_max_lanes(int k, int j, int N) {
+  uint64_t m = 0;
+  for (int l = 0; l < 64; ++l) {
+    const bool desc = (l & k) == 0 || k == N;
+    const bool lower = (l & j) == 0;
+    if (lower == desc) m |= 1ull << l;
+  }
+  return m;
+}
+
+// one compare-exchange step (k, j) of the bitonic sort of groups of N lanes
+template <int N, int k, int j>
+__device__ __forceinline__ float bitonic_step(float v, int lane) {
+  const float o = xor_lane(v, j, lane);
+  return ((o > v) == lane_in_here<bitonic_max_lanes(k, j, N)>()) ? o : v;
+}
+template <int N, int k, int j>
+__device__ __forceinline__ float bitonic_merge(float v, int lane) {
+  v = bitonic_step<N, k, j>(v, lane);
+  if constexpr (j > 1) v = bitonic_merge<N, k, j / 2>(v, lane);
+  return v;
+}
+template <int N, int k>
+__device__ __forceinline__ float bitonic_levels(float v, int lane) {
+  v = bitonic_merge<N, k, k / 2>(v, lane);
+  if constexpr (k < N) v = bitonic_levels<N, k * 2>(v, lane);
+  return v;
+}
 // Bitonic sort of one value per lane within groups of N lanes, descending.
 template <int N>
 __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
-#pragma unroll
-  for (int k = 2; k <= N; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const float o = xor_lane(v, j, lane);
-      const bool desc = (lane & k) == 0 || k == N;
-      const bool lower = (lane & j) == 0;
-      v = (lower == desc) ? fmaxf(v, o) : fminf(v, o);
-    }
-  }
-  return v;
+  return bitonic_levels<N, 2>(v, lane);
 }
 
 template <int LPT, int NLEV, bool HAS_BT>
@@ -198,53 +245,44 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool HAS_LM = NLEV >= 0;
   constexpr int NL = NLEV > 0 ? NLEV : 0;     // chain levels above the unigram root
   constexpr int NLA = NL > 0 ? NL : 1;        // array extent
-  constexpr int KCR = 16 / LPT;               // beams per chunk held in registers
+  constexpr int NF = NL > 1 ? NL - 1 : 1;     // backoff weights folded into an arc (extent)
+  constexpr int KCR = 16 / LPT;               // beams (key rows) per chunk
+  constexpr int NC = KCR * LPT;               // candidates per lane
+  // a chunk has at most 64 LM segments (beam, level): one lane each
+  constexpr int KSEG = (NL > 0 && KCR * NL > 64) ? 64 / (NL > 0 ? NL : 1) : KCR;
+  constexpr int kRowWords = 16;               // beam record per live position
 
   __shared__ __align__(16) uint32_t s_big[kBigWords];
-  // survivor buffer
-  __shared__ float s_bx[kCap];
-  __shared__ uint32_t s_bi[kCap], s_blm[kCap], s_bbt[kCap];
-  // ranked selection (fallback path and large-beam compaction)
-  __shared__ float s_nx[kMaxK];
-  __shared__ uint32_t s_ni[kMaxK], s_nlm[kMaxK], s_nbt[kMaxK];
-  // beams
-  __shared__ float s_score[kMaxK];
-  __shared__ int32_t s_last[kMaxK], s_len[kMaxK];
-  __shared__ uint64_t s_hash[kMaxK];
-  __shared__ uint32_t s_lms[kMaxK], s_bts[kMaxK];
-  __shared__ uint32_t s_lvb[kMaxK][NLA], s_lvc[kMaxK][NLA];
-  __shared__ float s_lvbo[kMaxK][NLA];
-  __shared__ uint32_t s_btb[kMaxK], s_btc[kMaxK];
-  __shared__ int32_t s_btpot[kMaxK];
-  // live list and chunks (positions in the live list)
-  __shared__ int32_t s_alive[kMaxK];
-  __shared__ int32_t s_hoff[kMaxK + 1], s_boff[kMaxK + 1];
-  __shared__ int32_t s_chunk[kMaxK + 1];
-  __shared__ int32_t s_nchunk;
-  // selection
+  // survivor pool: score bits, flat index, LM target (raw), boosting key
+  __shared__ uint4 s_pool[kCap];
+  // reserved regions (ping-pong): blank candidates, or the best K so far
+  __shared__ uint4 s_res[2][kMaxK];
+  // beam records by live position: score, last label, slot, pot, backoff weights
+  __shared__ __align__(16) uint32_t s_row[(kMaxK + 16) * kRowWords];
   __shared__ float s_top[kWaves * 8];
-  __shared__ int32_t s_order[kMaxK];
-  __shared__ uint64_t s_rkh[kMaxK];
-  __shared__ uint32_t s_rkm[kMaxK];
   __shared__ uint64_t s_red[2][kWaves];
   __shared__ int32_t s_nbuf, s_overflow;
-  __shared__ int32_t s_best;
+  __shared__ int32_t s_best, s_bestlen;
   __shared__ float s_bestscore;
+  // statistics (only with p.stats): alive beam-frames, LM chain states and
+  // arcs, boosting chain nodes and arcs, emitting winners
+  __shared__ unsigned long long s_st[6];
 
-  uint32_t* const lmkey = s_big + kOffLmKey;
-  uint32_t* const btkey = s_big + kOffBtKey;
-  float* const stv = reinterpret_cast<float*>(s_big + kOffStV);
-  uint32_t* const sttgt = s_big + kOffStTgt;
-  uint32_t* const stkey = s_big + kOffStKey;
-  uint32_t* const btclr = s_big + kOffBtClr;
+  uint64_t* const lmrow = reinterpret_cast<uint64_t*>(s_big);
+  uint32_t* const btrow = s_big + kOffBtRow;
+  uint32_t* const tgt = s_big + kOffTgt;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int b = blockIdx.x;
   const int V = p.V, W = V + 1, K = p.K, T = p.T;
-  const int kcmax = min(K, KCR);
+  const int kcmax = min(K, KSEG);
   const float alpha = p.alpha, beta = p.beta, boost_w = p.boost_w;
+  const uint64_t lmlt = lanemask_lt();
+  // lanes <= this lane, as two 32-bit halves
+  const uint32_t lmle_lo = lane >= 31 ? 0xFFFFFFFFu : ((2u << lane) - 1u);
+  const uint32_t lmle_hi = lane < 32 ? 0u : (lane == 63 ? 0xFFFFFFFFu : ((2u << (lane - 32)) - 1u));
 
   int L = p.lengths[b];
   uint32_t status = 0;
@@ -253,335 +291,409 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   const float* Db = p.logprobs + static_cast<size_t>(b) * T * W;
   int32_t* bpb = p.bp + static_cast<size_t>(b) * T * K;
 
-  // ---- per-lane constants and the first row ----
+  // ---- per-lane label constants and the first row ----
+  // lane owns labels c = tid + j*512; labels >= V score -inf through rD
   float rD[LPT], rDn[LPT], rP1[LPT];
-  uint32_t rRoot[LPT];
+  uint32_t rRoot[LPT], rcc[LPT];
 #pragma unroll
   for (int j = 0; j < LPT; ++j) {
     const int c = tid + j * kThreads;
     const bool ok = c < V;
+    rcc[j] = ok ? static_cast<uint32_t>(c) : 0u;
     rP1[j] = (HAS_LM && ok) ? p.lm_unigram[c] : 0.0f;
     rRoot[j] = (HAS_BT && ok) ? p.bt_root_key[c] : 0u;
-    rDn[j] = (ok && L > 0) ? Db[c] : 0.0f;
-    rD[j] = 0.0f;
+    rDn[j] = ok ? (L > 0 ? Db[c] : 0.0f) : kNegInf;
+    rD[j] = kNegInf;
   }
-  float rBlankN = (L > 0 && tid < K) ? Db[V] : 0.0f;
+  const bool blank_lane = (wave == 0) && (lane < K);
+  float rBlankN = (L > 0 && blank_lane) ? Db[V] : 0.0f;
   float rBlank = 0.0f;
 
-  // statistics (wave 0, lane = slot)
-  int64_t st_alive = 0, st_lms = 0, st_lma = 0, st_btn = 0, st_bta = 0, st_emit = 0;
-
-  // ---- initial beams and their chain headers (wave 0, lane j = slot j) ----
-  if (wave == 0) {
-    const int j = lane;
-    const bool alive = (j == 0);
-    int32_t acnt = 0, bcnt = 0;
-    if (j < K) {
-      s_score[j] = (j == 0) ? 0.0f : kNegInf;
-      s_last[j] = V;
-      s_len[j] = 0;
-      s_hash[j] = 0ull;
-      s_lms[j] = HAS_LM ? p.lm_bos_state : 0u;
-      s_bts[j] = 0u;
+  // ---- beam state: slot j in lane j, replicated in every wave ----
+  const int j = lane;
+  float sc = (j == 0) ? 0.0f : kNegInf;
+  int32_t last = V, len = 0;
+  uint64_t hash = 0ull;
+  uint32_t lms = HAS_LM ? p.lm_bos_state : 0u, bts = 0u;
+  uint32_t lvb[NLA], lvc[NLA];
+  float lvbo[NLA];
 #pragma unroll
-      for (int l = 0; l < NLA; ++l) {
-        s_lvb[j][l] = 0u;
-        s_lvc[j][l] = 0u;
-        s_lvbo[j][l] = 0.0f;
+  for (int l = 0; l < NLA; ++l) {
+    lvb[l] = 0u;
+    lvc[l] = 0u;
+    lvbo[l] = 0.0f;
+  }
+  uint32_t btb = 0u, btc = 0u;
+  int32_t btpot = 0;
+  bool alive = (j == 0);
+  const bool want_stats = p.stats != nullptr;
+  if (j == 0) {
+    if (HAS_LM) {
+#pragma unroll
+      for (int l = 0; l < NL; ++l) {
+        const LmLevel h = p.lm_states[static_cast<size_t>(p.lm_bos_state) * NL + l];
+        lvb[l] = h.begin;
+        lvc[l] = h.count;
+        lvbo[l] = h.bo;
       }
-      if (HAS_LM && alive) {
+    }
+    if (HAS_BT) {
+      const BtNode nd = p.bt_nodes[0];
+      btb = nd.list_begin;
+      btc = nd.list_count;
+      btpot = static_cast<int32_t>(nd.pot & 0xFFu);
+    }
+  }
+  // beam record of live position lp (written by wave 0 for the live slots)
+  auto put_row = [&](int lp) {
+    uint32_t* rr = s_row + lp * kRowWords;
+    *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc), static_cast<uint32_t>(last),
+                                               static_cast<uint32_t>(j), static_cast<uint32_t>(btpot));
+#pragma unroll
+    for (int l0 = 0; l0 < NL; l0 += 4) {
+      const auto bo_at = [&](int l) { return l < NL ? __float_as_uint(lvbo[l < NLA ? l : 0]) : 0u; };
+      *reinterpret_cast<uint4*>(rr + 4 + l0) = make_uint4(bo_at(l0), bo_at(l0 + 1), bo_at(l0 + 2), bo_at(l0 + 3));
+    }
+  };
+  // chunk plan: chunk id of each live slot, number of chunks (uniform)
+  int cid = 0;
+  int nch = 1;
+
+  for (int i = tid; i < kOffTgt; i += kThreads) s_big[i] = 0u;
+  for (int i = tid; i < (kMaxK + 16) * kRowWords; i += kThreads) s_row[i] = 0u;
+  __syncthreads();
+  if (tid == 0) {
+    put_row(0);
+    s_nbuf = 0;
+    s_overflow = 0;
+    if (want_stats) {
+      // the initial beam's chain is scanned in frame 0
+      unsigned long long ns = 0, na = 0;
+#pragma unroll
+      for (int l = 0; l < NL; ++l) {
+        if (L > 0 && (lvc[l] & kExists)) {
+          ns += 1;
+          na += lvc[l] & ~kExists;
+        }
+      }
+      s_st[0] = L > 0 ? 1 : 0;
+      s_st[1] = ns;
+      s_st[2] = na;
+      s_st[3] = 0;
+      s_st[4] = 0;
+      s_st[5] = 0;
+    }
+  }
+  uint32_t gen = 0u;
+  int mpar = 0;  // reserved region holding the pool's reserved entries
+  __syncthreads();
+
+  for (int t = 0; t < L; ++t) {
+    // ---- rotate and prefetch the log-prob row ----
+#pragma unroll
+    for (int jj = 0; jj < LPT; ++jj) rD[jj] = rDn[jj];
+    rBlank = rBlankN;
+    if (t + 1 < L) {
+      const float* rowp = Db + static_cast<size_t>(t + 1) * W;
+#pragma unroll
+      for (int jj = 0; jj < LPT; ++jj) {
+        const int c = tid + jj * kThreads;
+        if (c < V) rDn[jj] = __builtin_nontemporal_load(rowp + c);
+      }
+      if (blank_lane) rBlankN = __builtin_nontemporal_load(rowp + V);
+    }
+    float tau_run = kNegInf;
+    int nfin = 0;
+    int cs = 0;  // live position of the chunk's first beam
+
+    for (int ch = 0; ch < nch; ++ch) {
+      const bool inch = alive && (cid == ch);
+      const uint64_t chmask = __ballot(inch);
+      const int kc = __popcll(chmask);
+      const int row = __popcll(chmask & lmlt);
+
+      // ---- F. fill the key rows of this chunk ----
+      if (gen == kGenMax) {
+        // rows were last read before the previous filter barrier
+        for (int i = tid; i < kOffTgt; i += kThreads) s_big[i] = 0u;
+        __syncthreads();
+        gen = 0u;
+      }
+      ++gen;
+      const uint32_t genhi = gen << kGenShift;
+      if (HAS_LM && NL > 0) {
+        // Segment table, lane s = segment s: the non-empty (beam, level) arc
+        // runs of the chunk, level-major.  The chunk's arcs are numbered by
+        // their position in this concatenation, which is also their staging
+        // slot.  Fields: arc base, row | level << 8, and the backoff weights
+        // an arc of that level adds (bo of the levels above, then zeros).
+        int S = 0;
+        uint32_t sg_cnt = 0u, sg_base = 0u, sg_rl = 0u;
+        float sg_f[NF];
+#pragma unroll
+        for (int k = 0; k < NF; ++k) sg_f[k] = 0.0f;
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-          const LmLevel h = p.lm_states[static_cast<size_t>(p.lm_bos_state) * NL + l];
-          s_lvb[j][l] = h.begin;
-          s_lvc[j][l] = h.count;
-          s_lvbo[j][l] = h.bo;
-          acnt += static_cast<int32_t>(h.count & ~kExists);
-          if (L > 0 && (h.count & kExists)) {
-            st_lms += 1;
-            st_lma += h.count & ~kExists;
+          const uint32_t n = inch ? (lvc[l] & ~kExists) : 0u;
+          const uint64_t m = __ballot(n != 0u);
+          const int nl = __popcll(m);
+          if (nl > 0) {  // wave-uniform
+            // senders push to their segment lane; the rest to a lane outside
+            // [S, S + nl) (S + nl <= 64)
+            const int dst = (n != 0u) ? S + __popcll(m & lmlt) : ((S + nl) & 63);
+            const int addr = dst << 2;
+            const uint32_t r_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(n)));
+            const uint32_t r_base = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(lvb[l])));
+            const uint32_t r_rl =
+                static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, row | (l << 8)));
+            float r_f[NF];
+#pragma unroll
+            for (int k = 0; k + 1 < NL; ++k) {
+              const int lk = l + 1 + k;
+              const float fk = lk < NL ? lvbo[lk < NLA ? lk : 0] : 0.0f;
+              r_f[k] = __int_as_float(__builtin_amdgcn_ds_permute(addr, __float_as_int(fk)));
+            }
+            if (lane >= S && lane < S + nl) {
+              sg_cnt = r_cnt;
+              sg_base = r_base;
+              sg_rl = r_rl;
+#pragma unroll
+              for (int k = 0; k + 1 < NL; ++k) sg_f[k] = r_f[k];
+            }
+            S += nl;
+          }
+        }
+        const int sincl = wave_incl_scan(static_cast<int>(sg_cnt), lane);
+        const uint32_t sstart = static_cast<uint32_t>(sincl) - sg_cnt;
+        const uint32_t ntot = static_cast<uint32_t>(rdlane(sincl, 63));
+        const uint32_t sg_off = sg_base - sstart;  // arc index = sg_off + position
+        const bool sg_live = lane < S;
+        const int ntile = static_cast<int>((ntot + 63u) >> 6);
+        for (int t0 = wave; t0 < ntile; t0 += kWaves * kTileUnroll) {
+          LmArc a[kTileUnroll];
+          uint32_t arl[kTileUnroll];
+          float af[kTileUnroll][NF];
+#pragma unroll
+          for (int u = 0; u < kTileUnroll; ++u) {
+            const int tt = t0 + u * kWaves;
+            arl[u] = 0u;
+            a[u].token = 0xFFFFFFFFu;
+            if (tt < ntile) {  // wave-uniform
+              // tile = 64 consecutive positions; the segment of lane 0 plus
+              // the segments starting inside the tile give each lane's
+              const uint32_t q0 = static_cast<uint32_t>(tt) << 6;
+              const int s0 = __popcll(__ballot(sg_live && sstart <= q0)) - 1;
+              uint64_t bm = __ballot(sg_live && sstart > q0 && sstart < q0 + 64u);
+              uint64_t om = 0ull;
+              while (bm) {
+                const int sb = static_cast<int>(__builtin_ctzll(bm));
+                bm &= bm - 1ull;
+                om |= 1ull << (rdlane(sstart, sb) - q0);
+              }
+              const int seg = s0 + __popc(static_cast<uint32_t>(om) & lmle_lo) +
+                              __popc(static_cast<uint32_t>(om >> 32) & lmle_hi);
+              const int sa = seg << 2;
+              const uint32_t q = q0 + static_cast<uint32_t>(lane);
+              const uint32_t off = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(sa, static_cast<int>(sg_off)));
+              arl[u] = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(sa, static_cast<int>(sg_rl)));
+#pragma unroll
+              for (int k = 0; k + 1 < NL; ++k)
+                af[u][k] = __int_as_float(__builtin_amdgcn_ds_bpermute(sa, __float_as_int(sg_f[k])));
+              a[u] = p.lm_arcs[q < ntot ? off + q : 0u];
+            }
+          }
+#pragma unroll
+          for (int u = 0; u < kTileUnroll; ++u) {
+            const uint32_t q = (static_cast<uint32_t>(t0 + u * kWaves) << 6) + static_cast<uint32_t>(lane);
+            // positions past the chunk's arcs (and tiles past the last) skip
+            if (q < ntot && a[u].token < static_cast<uint32_t>(V)) {
+              float v = a[u].logp;
+#pragma unroll
+              for (int k = 0; k + 1 < NL; ++k) v = v + af[u][k];
+              const float av = alpha * v;
+              tgt[q] = a[u].target;
+              const uint32_t hi = genhi | (((arl[u] >> 8) + 1u) << 23) | q;
+              atomicMax(reinterpret_cast<unsigned long long*>(&lmrow[(arl[u] & 0xFFu) * V + a[u].token]),
+                        (static_cast<unsigned long long>(hi) << 32) | __float_as_uint(av));
+            }
           }
         }
       }
       if (HAS_BT) {
-        const BtNode nd = p.bt_nodes[0];
-        s_btb[j] = nd.list_begin;
-        s_btc[j] = nd.list_count;
-        s_btpot[j] = static_cast<int32_t>(nd.pot & 0xFFu);
-        if (alive) bcnt = static_cast<int32_t>(nd.list_count);
-      } else {
-        s_btpot[j] = 0;
-      }
-    }
-    if (alive && L > 0) st_alive += 1;
-    if (j == 0) {
-      s_alive[0] = 0;
-      s_hoff[0] = 0;
-      s_hoff[1] = acnt;
-      s_boff[0] = 0;
-      s_boff[1] = bcnt;
-      s_chunk[0] = 0;
-      s_chunk[1] = 1;
-      s_nchunk = 1;
-      s_nbuf = 0;
-      s_overflow = 0;
-    }
-    if (j < K) {
-      s_bx[kChunkCap + j] = kNegInf;
-      s_bi[kChunkCap + j] = 0xFFFFFFFFu;
-    }
-  }
-  for (int i = tid; i < kKeyWords; i += kThreads) {
-    if (HAS_LM) lmkey[i] = 0u;
-    if (HAS_BT) btkey[i] = 0u;
-  }
-  __syncthreads();
-
-  for (int t = 0; t < L; ++t) {
-    // ---- 1. rotate and prefetch the log-prob row ----
+        // same scheme, one segment per beam (its merged continuation list)
+        const uint32_t nb = inch ? btc : 0u;
+        const uint64_t m = __ballot(nb != 0u);
+        const int S = __popcll(m);
+        if (S > 0) {  // wave-uniform
+          const int dst = (nb != 0u) ? __popcll(m & lmlt) : (S & 63);
+          const int addr = dst << 2;
+          uint32_t bg_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(nb)));
+          const uint32_t bg_base = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(btb)));
+          const uint32_t bg_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, row));
+          const bool bg_live = lane < S;
+          if (!bg_live) bg_cnt = 0u;
+          const int bincl = wave_incl_scan(static_cast<int>(bg_cnt), lane);
+          const uint32_t bstart = static_cast<uint32_t>(bincl) - bg_cnt;
+          const uint32_t nbt = static_cast<uint32_t>(rdlane(bincl, 63));
+          const uint32_t bg_off = bg_base - bstart;
+          const int ntile = static_cast<int>((nbt + 63u) >> 6);
+          for (int t0 = wave; t0 < ntile; t0 += kWaves * kTileUnroll) {
+            BtEntry e[kTileUnroll];
+            uint32_t erow[kTileUnroll];
 #pragma unroll
-    for (int j = 0; j < LPT; ++j) rD[j] = rDn[j];
-    rBlank = rBlankN;
-    if (t + 1 < L) {
-      const float* row = Db + static_cast<size_t>(t + 1) * W;
-#pragma unroll
-      for (int j = 0; j < LPT; ++j) {
-        const int c = tid + j * kThreads;
-        if (c < V) rDn[j] = __builtin_nontemporal_load(row + c);
-      }
-      if (tid < K) rBlankN = __builtin_nontemporal_load(row + V);
-    }
-    // s_nbuf, s_overflow and the reserved blank slots were reset by the
-    // previous frame's update (or the initialisation)
-    float tau = kNegInf;
-    const int nchunk = s_nchunk;
-
-    for (int ch = 0; ch < nchunk; ++ch) {
-      const int cs = s_chunk[ch];
-      const int kc = s_chunk[ch + 1] - cs;
-      const int hbase = s_hoff[cs];
-      const int bbase = s_boff[cs];
-      const int lm_total = min(s_hoff[cs + kc] - hbase, kLmStage);
-      const int bt_total = min(s_boff[cs + kc] - bbase, kBtStage);
-
-      // ---- 2. fill: one wave per beam ----
-      for (int i = wave; i < kc; i += kWaves) {
-        const int k = s_alive[cs + i];
-        const uint32_t rowbase = static_cast<uint32_t>(i) * static_cast<uint32_t>(V);
-        if (HAS_LM && NL > 0) {
-          const int hoff = s_hoff[cs + i] - hbase;
-          uint32_t lb[NLA], lend[NLA];
-          float lbo[NLA];
-          uint32_t run = 0;
-#pragma unroll
-          for (int l = 0; l < NL; ++l) {
-            lb[l] = s_lvb[k][l];
-            run += s_lvc[k][l] & ~kExists;
-            lend[l] = run;
-            lbo[l] = s_lvbo[k][l];
-          }
-          const int total = static_cast<int>(run);
-          for (int r0 = 0; r0 < total; r0 += 64 * kFillUnroll) {
-            LmArc a[kFillUnroll];
-            int lv[kFillUnroll];
-#pragma unroll
-            for (int u = 0; u < kFillUnroll; ++u) {
-              lv[u] = -1;
-              if (r0 + u * 64 >= total) continue;  // wave-uniform
-              const uint32_t q = static_cast<uint32_t>(r0 + u * 64 + lane);
-              int l = 0;
-              uint32_t start = 0, base = lb[0];
-#pragma unroll
-              for (int m = 0; m + 1 < NL; ++m) {
-                if (q >= lend[m]) {
-                  l = m + 1;
-                  start = lend[m];
-                  base = lb[m + 1];
+            for (int u = 0; u < kTileUnroll; ++u) {
+              const int tt = t0 + u * kWaves;
+              erow[u] = 0u;
+              e[u].token = 0xFFFFFFFFu;
+              if (tt < ntile) {  // wave-uniform
+                const uint32_t q0 = static_cast<uint32_t>(tt) << 6;
+                const int s0 = __popcll(__ballot(bg_live && bstart <= q0)) - 1;
+                uint64_t bm = __ballot(bg_live && bstart > q0 && bstart < q0 + 64u);
+                uint64_t om = 0ull;
+                while (bm) {
+                  const int sb = static_cast<int>(__builtin_ctzll(bm));
+                  bm &= bm - 1ull;
+                  om |= 1ull << (rdlane(bstart, sb) - q0);
                 }
-              }
-              const bool ok = q < static_cast<uint32_t>(total);
-              lv[u] = ok ? l : -1;
-              a[u] = p.lm_arcs[ok ? base + (q - start) : lb[0]];
-            }
-#pragma unroll
-            for (int u = 0; u < kFillUnroll; ++u) {
-              if (r0 + u * 64 >= total) continue;  // wave-uniform
-              if (lv[u] >= 0) {
-                const int q = r0 + u * 64 + lane;
-                float v = a[u].logp;
-#pragma unroll
-                for (int l2 = 1; l2 < NL; ++l2)
-                  if (l2 > lv[u]) v = v + lbo[l2];
-                const float av = alpha * v;
-                const int pos = hoff + q;
-                // </s> (token V) is never a frame label; it is read at the end
-                const bool tok_ok = a[u].token < static_cast<uint32_t>(V) && pos < kLmStage;
-                const uint32_t kidx = rowbase + (tok_ok ? a[u].token : 0u);
-                if (pos < kLmStage) {
-                  stv[pos] = av;
-                  sttgt[pos] = a[u].target;
-                  stkey[pos] = kidx;
-                }
-                if (tok_ok)
-                  atomicMax(&lmkey[kidx], (static_cast<uint32_t>(lv[u] + 1) << 28) | static_cast<uint32_t>(pos));
+                const int seg = s0 + __popc(static_cast<uint32_t>(om) & lmle_lo) +
+                                __popc(static_cast<uint32_t>(om >> 32) & lmle_hi);
+                const int sa = seg << 2;
+                const uint32_t q = q0 + static_cast<uint32_t>(lane);
+                const uint32_t off = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(sa, static_cast<int>(bg_off)));
+                erow[u] = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(sa, static_cast<int>(bg_row)));
+                e[u] = p.bt_list[q < nbt ? off + q : 0u];
               }
             }
-          }
-        }
-        if (HAS_BT) {
-          const int boff = s_boff[cs + i] - bbase;
-          const uint32_t lbeg = s_btb[k];
-          const int cnt = static_cast<int>(s_btc[k]);
-          for (int r0 = 0; r0 < cnt; r0 += 64 * 4) {
-            BtEntry e[4];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const int q = r0 + u * 64 + lane;
-              e[u] = p.bt_list[lbeg + (q < cnt ? q : 0)];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const int q = r0 + u * 64 + lane;
-              if (q < cnt && boff + q < kBtStage) {
-                const uint32_t kidx = rowbase + e[u].token;
-                btkey[kidx] = e[u].key;
-                btclr[boff + q] = kidx;
-              }
-            }
+            for (int u = 0; u < kTileUnroll; ++u)
+              if (((static_cast<uint32_t>(t0 + u * kWaves) << 6) + static_cast<uint32_t>(lane)) < nbt &&
+                  e[u].token < static_cast<uint32_t>(V))
+                btrow[erow[u] * V + e[u].token] = (e[u].key & kLowMask) | genhi;
           }
         }
       }
-      __syncthreads();
-      // stable until the filter below appends (nobody writes s_nbuf between
-      // the barrier above and the barrier that follows the bound)
-      const int nbuf_before = s_nbuf;
+      __syncthreads();  // A: rows complete
 
-      // ---- 3. candidates ----
-      // beam i of the chunk lives in lane i; its data is broadcast per beam
-      // with readlane so the scoring below is straight-line code
-      const int hrow = lane < kc ? lane : 0;
-      const int hk = s_alive[cs + hrow];
-      const float hsc = lane < kc ? s_score[hk] : kNegInf;
-      const int hlast = s_last[hk];
-      float hbo[NLA];
-#pragma unroll
-      for (int l = 0; l < NL; ++l) hbo[l] = s_lvbo[hk][l];
-      const int hpot = HAS_BT ? s_btpot[hk] : 0;
-      float cand[16];
+      // ---- C. candidates ----
+      // chunk row i is live position cs + i; its beam record is read with
+      // broadcast LDS loads so the scoring is straight-line code
       int kslot[KCR];
+      float ksc[KCR];
+      int klast[KCR];
+      float kbo[KCR][NLA];
+      int kpot[KCR];
+#pragma unroll
+      for (int i = 0; i < KCR; ++i) {
+        const uint32_t* rr = s_row + (cs + i) * kRowWords;
+        const uint4 h0 = *reinterpret_cast<const uint4*>(rr);
+        ksc[i] = (i < kc) ? __uint_as_float(h0.x) : kNegInf;
+        klast[i] = static_cast<int>(h0.y);
+        kslot[i] = static_cast<int>(h0.z);
+        kpot[i] = static_cast<int>(h0.w);
+#pragma unroll
+        for (int l0 = 0; l0 < NL; l0 += 4) {
+          const uint4 h = *reinterpret_cast<const uint4*>(rr + 4 + l0);
+          const uint32_t hv[4] = {h.x, h.y, h.z, h.w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            if (l0 + q < NL) kbo[i][(l0 + q) < NLA ? (l0 + q) : 0] = __uint_as_float(hv[q]);
+        }
+      }
+      float cand[NC];
+      uint32_t lhi[NC], bkr[NC];
       float lmax = kNegInf;
 #pragma unroll
       for (int i = 0; i < KCR; ++i) {
-        kslot[i] = __builtin_amdgcn_readlane(hk, i);
-        const float sk = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(hsc), i));
-        const int lastk = __builtin_amdgcn_readlane(hlast, i);
-        float bo[NLA];
 #pragma unroll
-        for (int l = 0; l < NL; ++l) bo[l] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(hbo[l]), i));
-        const int potk = HAS_BT ? __builtin_amdgcn_readlane(hpot, i) : 0;
-#pragma unroll
-        for (int j = 0; j < LPT; ++j) {
-          const int c = tid + j * kThreads;
-          // beams beyond the chunk score -inf (sk = -inf)
-          const float x0 = sk + rD[j];
+        for (int jj = 0; jj < LPT; ++jj) {
+          const int r = i * LPT + jj;
+          const int c = tid + jj * kThreads;
+          const uint32_t e = static_cast<uint32_t>(i * V) + rcc[jj];
+          const float x0 = ksc[i] + rD[jj];
           float x1 = x0 + beta;
+          lhi[r] = 0u;
+          bkr[r] = 0u;
           if (HAS_LM) {
-            const uint32_t key = lmkey[i * V + c];
-            const float sv = stv[key & 0x0FFFFFFFu];
-            float v = rP1[j];
+            const uint64_t ent = lmrow[e];
+            const uint32_t hi = static_cast<uint32_t>(ent >> 32);
+            float v = rP1[jj];
 #pragma unroll
-            for (int l = 0; l < NL; ++l) v = v + bo[l];
-            const float av = (key != 0u) ? sv : alpha * v;
+            for (int l = 0; l < NL; ++l) v = v + kbo[i][l];
+            const bool has = hi >= genhi;
+            const float av = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
             x1 = x1 + av;
+            lhi[r] = has ? hi : 0u;
           }
           if (HAS_BT) {
-            uint32_t bk = btkey[i * V + c];
-            bk = (bk != 0u) ? bk : rRoot[j];
+            const uint32_t be = btrow[e];
+            const uint32_t bk = (be >= genhi) ? be : rRoot[jj];
             const int pre = static_cast<int>((bk >> 20) & 63u);
-            const float bv = boost_w * static_cast<float>(pre - potk);
+            const float bv = boost_w * static_cast<float>(pre - kpot[i]);
             x1 = x1 + bv;
+            bkr[r] = bk;
           }
-          float x = (c != lastk) ? x1 : x0;
-          x = (c < V) ? x : kNegInf;
-          cand[i * LPT + j] = x;
+          const float x = (c != klast[i]) ? x1 : x0;
+          cand[r] = x;
           lmax = fmaxf(lmax, x);
         }
       }
-
-      // ---- 4a. lower bound on the K-th best ----
+      if (ch == 0 && blank_lane) {
+        // blank candidates of every slot into the reserved region
+        const float x = sc + rBlank;
+        const bool ok = sc != kNegInf && x != kNegInf;
+        s_res[mpar][j] = make_uint4(__float_as_uint(ok ? x : kNegInf),
+                                    ok ? static_cast<uint32_t>(j * W + V) : 0xFFFFFFFFu, 0u, 0u);
+      }
+      if (tid == 0) {
+        s_nbuf = 0;  // the previous rank read it before barrier D
+        s_overflow = 0;
+      }
       // Maxima of disjoint lane groups are distinct candidates, so the K-th
       // largest of at least K group maxima bounds the K-th best candidate
       // from below.  K <= 32: the 32 rows of 16 lanes; otherwise 64 groups of
       // 8 lanes.
-      {
-        if (K <= 32) {
-          const float g = row_max_last(lmax);
-          if ((lane & 15) == 15) s_top[wave * 4 + (lane >> 4)] = g;
-        } else {
-          const float g = group8_max(lmax, lane);
-          if ((lane & 7) == 7) s_top[wave * 8 + (lane >> 3)] = g;
-        }
+      if (K <= 32) {
+        const float g = row_max_last(lmax);
+        if ((lane & 15) == 15) s_top[wave * 4 + (lane >> 4)] = g;
+      } else {
+        const float g = group8_max(lmax, lane);
+        if ((lane & 7) == 7) s_top[wave * 8 + (lane >> 3)] = g;
       }
-      __syncthreads();
+      __syncthreads();  // B: bound inputs, blanks, pool reset
+
+      // ---- T. bound and filter ----
       {
         float tc;
         if (K <= 32) {
           const float v = wave_sort_desc<32>(lane < 32 ? s_top[lane] : kNegInf, lane);
-          tc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), K - 1));
+          tc = rdlane(v, K - 1);
         } else {
           const float v = wave_sort_desc<64>(s_top[lane], lane);
-          tc = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), K - 1));
+          tc = rdlane(v, K - 1);
         }
-        tau = fmaxf(tau, tc);
-      }
-
-      // ---- 4b. filter and append survivors (and, once, the blank candidates) ----
-      {
-        const bool last_chunk_f = (ch + 1 == nchunk);
+        const float tau = fmaxf(tau_run, tc);
         uint32_t qmask = 0u;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) qmask |= (cand[r] >= tau && cand[r] != kNegInf) ? (1u << r) : 0u;
+        for (int r = 0; r < NC; ++r) qmask |= (cand[r] >= tau && cand[r] != kNegInf) ? (1u << r) : 0u;
         const int mycnt = __popc(qmask);
         const int incl = wave_incl_scan(mycnt, lane);
-        const int wtotal = __builtin_amdgcn_readlane(incl, 63);
-        int wbase = 0;
-        if (lane == 0 && wtotal > 0) wbase = atomicAdd(&s_nbuf, wtotal);
-        wbase = __builtin_amdgcn_readfirstlane(wbase);
+        const int wtotal = rdlane(incl, 63);
         if (wtotal > 0) {
+          int wbase = 0;
+          if (lane == 0) wbase = atomicAdd(&s_nbuf, wtotal);
+          wbase = __builtin_amdgcn_readfirstlane(wbase);
           int slot = wbase + incl - mycnt;
-          uint32_t rem = qmask;
-          while (__ballot(rem != 0u)) {  // wave-uniform: max survivors of a lane
-            if (rem != 0u) {
-              const int r = __builtin_ctz(rem);
-              rem &= rem - 1u;
-              float x = cand[0];
 #pragma unroll
-              for (int rr = 1; rr < 16; ++rr) x = (r == rr) ? cand[rr] : x;
-              const int i = r / LPT, j = r % LPT;
-              const int c = tid + j * kThreads;
-              int k = kslot[0];
-#pragma unroll
-              for (int ii = 1; ii < KCR; ++ii) k = (i == ii) ? kslot[ii] : k;
-              uint32_t root = rRoot[0];
-#pragma unroll
-              for (int jj = 1; jj < LPT; ++jj) root = (j == jj) ? rRoot[jj] : root;
-              if (slot < kChunkCap) {
-                uint32_t lmt = 0u, bk = 0u;
-                if (HAS_LM) {
-                  const uint32_t kl = lmkey[i * V + c];
-                  // the last chunk leaves the staged target to the selection
-                  // (the staging survives until the next fill)
-                  lmt = last_chunk_f ? (kl != 0u ? (kl | 0x80000000u) : static_cast<uint32_t>(c))
-                                     : (kl != 0u ? sttgt[kl & 0x0FFFFFFFu] : static_cast<uint32_t>(c));
-                }
-                if (HAS_BT) {
-                  const uint32_t kb = btkey[i * V + c];
-                  bk = kb != 0u ? kb : root;
-                }
-                s_bx[slot] = x;
-                s_bi[slot] = static_cast<uint32_t>(k * W + c);
-                s_blm[slot] = lmt;
-                s_bbt[slot] = bk;
+          for (int r = 0; r < NC; ++r) {
+            if (qmask & (1u << r)) {
+              if (slot < kCap) {
+                const int i = r / LPT, jj = r % LPT;
+                const int c = tid + jj * kThreads;
+                // LM target: staged entry (resolved by the rank) or the
+                // token's unigram state
+                const uint32_t lraw = HAS_LM ? (lhi[r] != 0u ? lhi[r] : static_cast<uint32_t>(c)) : 0u;
+                s_pool[slot] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lraw,
+                                          bkr[r]);
               } else {
                 s_overflow = 1;
               }
@@ -589,465 +701,306 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
           }
         }
-        if (ch == 0 && tid < K) {
-          const float sk = s_score[tid];
-          const float x = sk + rBlank;
-          if (sk != kNegInf && x != kNegInf && x >= tau) {
-            const int bs = kChunkCap + tid;  // reserved blank slots
-            s_bx[bs] = x;
-            s_bi[bs] = static_cast<uint32_t>(tid * W + V);
-            s_blm[bs] = 0u;
-            s_bbt[bs] = 0u;
-          }
-        }
       }
-      __syncthreads();
+      __syncthreads();  // C: pool complete
 
-      // ---- 4c. overflow: exact extraction over (buffer before) U (chunk) ----
-      if (s_overflow) {
-        uint64_t prev = ~0ull;
-        int nk = 0;
-        for (int it = 0; it < K; ++it) {
-          uint64_t best = 0ull;
-          int who = -1;  // -1 none, 0..15 register, 100+e buffer
+      // ---- R. exact rank of the pool: reserved region P + survivors ----
+      {
+        const int P = mpar, Q = mpar ^ 1;
+        if (!s_overflow) {
+          const int n = min(s_nbuf, kCap);
+          const int N = K + n;
+          nfin = 0;
+          if (N <= 64) {
+            // one entry per lane; this wave ranks entries wave + 8u
+            uint4 eq = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+            if (lane < N) eq = (lane < K) ? s_res[P][lane] : s_pool[lane - K];
+            const float xq = __uint_as_float(eq.x);
+            nfin = __popcll(__ballot(xq != kNegInf));
+            int myrank = K;
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            if (cand[r] != kNegInf) {
-              const int i = r / LPT, j = r % LPT;
-              const int c = tid + j * kThreads;
-              const int k = s_alive[cs + i];
-              const uint64_t key = order_key(cand[r], static_cast<uint32_t>(k * W + c));
-              if (key < prev && key > best) { best = key; who = r; }
+            for (int u = 0; u < 8; ++u) {
+              const int ql = wave + u * kWaves;
+              const float xs = rdlane(xq, ql);
+              const uint32_t is = rdlane(eq.y, ql);
+              const int rk = __popcll(__ballot(xq > xs || (xq == xs && eq.y < is)));
+              myrank = ((lane >> 3) == u) ? rk : myrank;
             }
-          }
-          for (int e = tid; e < nbuf_before; e += kThreads) {
-            const uint64_t key = order_key(s_bx[e], s_bi[e]);
-            if (key < prev && key > best) { best = key; who = 100 + e; }
-          }
-          uint64_t wbest = best;
-          for (int off = 1; off < 64; off <<= 1) {
-            const uint64_t o = __shfl_xor(wbest, off);
-            wbest = o > wbest ? o : wbest;
-          }
-          if (lane == 0) s_red[it & 1][wave] = wbest;
-          __syncthreads();
-          uint64_t gbest = s_red[it & 1][0];
+            if ((lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf) {
+              uint32_t lmt = eq.z;
+              if (HAS_LM && lane >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+              s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
+            }
+          } else
+          // blocks of 64 entries: this wave ranks entries qb + (wave + 8u)
+          // against every entry, lane f holding entry fb + f
+          for (int qb = 0; qb < N; qb += 64) {
+            const int q = qb + lane;
+            uint4 eq = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+            if (q < N) eq = (q < K) ? s_res[P][q] : s_pool[q - K];
+            const float xq = __uint_as_float(eq.x);
+            nfin += __popcll(__ballot(xq != kNegInf));
+            int rk[8];
 #pragma unroll
-          for (int w = 1; w < kWaves; ++w) gbest = s_red[it & 1][w] > gbest ? s_red[it & 1][w] : gbest;
-          if (gbest == 0ull) break;  // nothing finite left (uniform)
-          if (who >= 0 && best == gbest) {
-            if (who < 100) {
-              const int r = who;
-              const int i = r / LPT, j = r % LPT;
-              const int c = tid + j * kThreads;
-              const int k = s_alive[cs + i];
-              uint32_t lmt = 0u, bk = 0u;
-              if (HAS_LM) {
-                const uint32_t key = lmkey[i * V + c];
-                lmt = (key != 0u) ? sttgt[key & 0x0FFFFFFFu] : static_cast<uint32_t>(c);
+            for (int u = 0; u < 8; ++u) rk[u] = 0;
+            for (int fb = 0; fb < N; fb += 64) {
+              float xf = xq;
+              uint32_t iff = eq.y;
+              if (fb != qb) {
+                const int f = fb + lane;
+                uint4 ef = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+                if (f < N) ef = (f < K) ? s_res[P][f] : s_pool[f - K];
+                xf = __uint_as_float(ef.x);
+                iff = ef.y;
               }
-              if (HAS_BT) {
-                bk = btkey[i * V + c];
-                if (bk == 0u) bk = rRoot[j];
+#pragma unroll
+              for (int u = 0; u < 8; ++u) {
+                const int ql = wave + u * kWaves;
+                if (qb + ql < N) {  // wave-uniform
+                  const float xs = rdlane(xq, ql);
+                  const uint32_t is = rdlane(eq.y, ql);
+                  rk[u] += __popcll(__ballot(xf > xs || (xf == xs && iff < is)));
+                }
               }
-              s_nx[it] = cand[r];
-              s_ni[it] = static_cast<uint32_t>(k * W + c);
-              s_nlm[it] = lmt;
-              s_nbt[it] = bk;
-            } else {
-              const int e = who - 100;
-              uint32_t lmt = s_blm[e];
-              if (HAS_LM && (lmt & 0x80000000u)) lmt = sttgt[lmt & 0x0FFFFFFFu];
-              s_nx[it] = s_bx[e];
-              s_ni[it] = s_bi[e];
-              s_nlm[it] = lmt;
-              s_nbt[it] = s_bbt[e];
+            }
+            // owner lane wave + 8u takes rank u
+            int myrank = K;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) myrank = ((lane >> 3) == u) ? rk[u] : myrank;
+            if ((lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf) {
+              uint32_t lmt = eq.z;
+              if (HAS_LM && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+              s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
             }
           }
-          prev = gbest;
-          ++nk;
-        }
-        __syncthreads();
-        for (int e = tid; e < nk; e += kThreads) {
-          s_bx[e] = s_nx[e];
-          s_bi[e] = s_ni[e];
-          s_blm[e] = s_nlm[e];
-          s_bbt[e] = s_nbt[e];
-        }
-        if (nk == K) tau = s_nx[K - 1];
-        __syncthreads();
-        if (tid == 0) {
-          s_nbuf = nk;
-          s_overflow = 0;
-        }
-      }
-
-      const bool last_chunk = (ch + 1 == nchunk);
-      if (!last_chunk) {
-        // ---- clear this chunk's key rows, then compact between chunks ----
-        if (HAS_LM)
-          for (int q = tid; q < lm_total; q += kThreads) lmkey[stkey[q]] = 0u;
-        if (HAS_BT)
-          for (int q = tid; q < bt_total; q += kThreads) btkey[btclr[q]] = 0u;
-        __syncthreads();
-        const int n = min(s_nbuf, kChunkCap);
-        if (n > K) {
-          for (int e = tid; e < n; e += kThreads) {
-            const float xe = s_bx[e];
-            const uint32_t ie = s_bi[e];
-            int rank = 0;
-            for (int f = 0; f < n; ++f) rank += beats(s_bx[f], s_bi[f], xe, ie) ? 1 : 0;
-            if (rank < K) {
-              s_nx[rank] = xe;
-              s_ni[rank] = ie;
-              s_nlm[rank] = s_blm[e];
-              s_nbt[rank] = s_bbt[e];
+        } else {
+          // exact extraction over (reserved region P) U (this chunk's candidates)
+          uint64_t prev = ~0ull;
+          int nk = 0;
+          for (int it = 0; it < K; ++it) {
+            uint64_t best = 0ull;
+            int who = -1;  // -1 none, 0..NC-1 register, 100+e reserved entry
+#pragma unroll
+            for (int r = 0; r < NC; ++r) {
+              if (cand[r] != kNegInf) {
+                const int i = r / LPT, jj = r % LPT;
+                const int c = tid + jj * kThreads;
+                const uint64_t key = order_key(cand[r], static_cast<uint32_t>(kslot[i] * W + c));
+                if (key < prev && key > best) {
+                  best = key;
+                  who = r;
+                }
+              }
             }
+            if (tid < K) {
+              const uint4 e = s_res[P][tid];
+              const float xe = __uint_as_float(e.x);
+              if (xe != kNegInf) {
+                const uint64_t key = order_key(xe, e.y);
+                if (key < prev && key > best) {
+                  best = key;
+                  who = 100 + tid;
+                }
+              }
+            }
+            uint64_t wbest = best;
+            for (int off = 1; off < 64; off <<= 1) {
+              const uint64_t o = __shfl_xor(wbest, off);
+              wbest = o > wbest ? o : wbest;
+            }
+            if (lane == 0) s_red[it & 1][wave] = wbest;
+            __syncthreads();
+            uint64_t gbest = s_red[it & 1][0];
+#pragma unroll
+            for (int w = 1; w < kWaves; ++w) gbest = s_red[it & 1][w] > gbest ? s_red[it & 1][w] : gbest;
+            if (gbest == 0ull) break;  // nothing finite left (uniform)
+            if (who >= 0 && best == gbest) {
+              if (who < 100) {
+                const int r = who;
+                const int i = r / LPT, jj = r % LPT;
+                const int c = tid + jj * kThreads;
+                uint32_t lmt = 0u;
+                if (HAS_LM) lmt = lhi[r] != 0u ? tgt[lhi[r] & 0xFFFu] : static_cast<uint32_t>(c);
+                s_res[Q][it] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lmt,
+                                          bkr[r]);
+              } else {
+                s_res[Q][it] = s_res[P][who - 100];
+              }
+            }
+            prev = gbest;
+            ++nk;
           }
-          __syncthreads();
-          for (int e = tid; e < K; e += kThreads) {
-            s_bx[e] = s_nx[e];
-            s_bi[e] = s_ni[e];
-            s_blm[e] = s_nlm[e];
-            s_bbt[e] = s_nbt[e];
-          }
-          tau = fmaxf(tau, s_nx[K - 1]);
-          __syncthreads();
-          if (tid == 0) s_nbuf = K;
-          __syncthreads();
+          nfin = nk;
         }
-      } else if (wave != 0) {
-        // the key rows are cleared by waves 1..7 while wave 0 selects
-        if (HAS_LM)
-          for (int q = tid - 64; q < lm_total; q += kThreads - 64) lmkey[stkey[q]] = 0u;
-        if (HAS_BT)
-          for (int q = tid - 64; q < bt_total; q += kThreads - 64) btkey[btclr[q]] = 0u;
+        // ranks [nfin, K) hold no candidate (the next chunk reads all K)
+        if (wave == 0 && lane >= nfin && lane < K) s_res[Q][lane] = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
       }
+      __syncthreads();  // D: best K of the chunk in region Q
+      mpar ^= 1;
+      if (nfin >= K) tau_run = fmaxf(tau_run, __uint_as_float(s_res[mpar][K - 1].x));
+      cs += kc;
     }
 
-    // ---- 5. selection and beam update ----
-    // survivors: s_b*[0, nlab) from the labels, s_b*[kChunkCap, kChunkCap+K) blanks
-    const int nlab = min(s_nbuf, kChunkCap);
-    const bool small = (nlab + K) <= 64;
-    if (!small) {
-      // exact ranking in LDS by every thread (large beams, rare otherwise)
-      const int n = nlab + K;
-      for (int e = tid; e < n; e += kThreads) {
-        const int ee = e < nlab ? e : kChunkCap + (e - nlab);
-        const float xe = s_bx[ee];
-        const uint32_t ie = s_bi[ee];
-        if (ie != 0xFFFFFFFFu) {
-          int rank = 0;
-          for (int f = 0; f < n; ++f) {
-            const int ff = f < nlab ? f : kChunkCap + (f - nlab);
-            const uint32_t iff = s_bi[ff];
-            rank += (iff != 0xFFFFFFFFu && beats(s_bx[ff], iff, xe, ie)) ? 1 : 0;
-          }
-          if (rank < K) {
-            uint32_t lmt = s_blm[ee];
-            if (HAS_LM && (lmt & 0x80000000u)) lmt = sttgt[lmt & 0x0FFFFFFFu];
-            s_nx[rank] = xe;
-            s_ni[rank] = ie;
-            s_nlm[rank] = lmt;
-            s_nbt[rank] = s_bbt[ee];
-          }
-        }
-      }
-      if (tid < K) {
-        // count of valid entries decides how many ranks were written
-        int cnt = 0;
-        for (int f = 0; f < n; ++f) {
-          const int ff = f < nlab ? f : kChunkCap + (f - nlab);
-          cnt += s_bi[ff] != 0xFFFFFFFFu ? 1 : 0;
-        }
-        if (tid >= cnt) s_ni[tid] = 0xFFFFFFFFu;
-      }
-      __syncthreads();
-    }
-    if (wave == 0) {
-      const int j = lane;
-      // candidate held by this lane before/after ranking
-      float x;
-      uint32_t idx;
-      int src = lane;
-      uint32_t lmt = 0u, btk = 0u;
-      LmLevel hh[NLA];
-      BtNode nd{0u, 0u, 0u, 0u};
-      if (small) {
-        // lane e holds survivor e (label survivors, then the blank slots)
-        const int n = nlab + K;
-        const int ee = j < nlab ? j : (j < n ? kChunkCap + (j - nlab) : -1);
-        float xe = kNegInf;
-        uint32_t ie = 0xFFFFFFFFu, lmt_e = 0u, btk_e = 0u;
-        if (ee >= 0) {
-          xe = s_bx[ee];
-          ie = s_bi[ee];
-          lmt_e = s_blm[ee];
-          btk_e = s_bbt[ee];
-        }
-        const bool valid_e = xe != kNegInf;
-        if (HAS_LM && valid_e && (lmt_e & 0x80000000u)) lmt_e = sttgt[lmt_e & 0x0FFFFFFFu];
-        // prefetch the chain headers of emitting survivors before ranking
-        const uint32_t vpar = valid_e ? ie / static_cast<uint32_t>(W) : 0u;
-        const int vc = valid_e ? static_cast<int>(ie - vpar * W) : V;
-        const bool vemit = valid_e && vc != V && vc != s_last[vpar];
-#pragma unroll
-        for (int l = 0; l < NL; ++l) hh[l] = p.lm_states[static_cast<size_t>(vemit ? lmt_e : p.lm_bos_state) * NL + l];
-        if (HAS_BT) nd = p.bt_nodes[vemit ? (btk_e & kBtChildMask) : 0u];
-        // rank = number of survivors that beat this one (broadcast reads)
-        int rank = 0;
-        // label survivors, 8 at a time (independent broadcast reads), then blanks
-        for (int f0 = 0; f0 < nlab; f0 += 8) {
-          float fx[8];
-          uint32_t fi[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            fx[u] = s_bx[f0 + u];
-            fi[u] = s_bi[f0 + u];
-          }
-#pragma unroll
-          for (int u = 0; u < 8; ++u) rank += (f0 + u < nlab && beats(fx[u], fi[u], xe, ie)) ? 1 : 0;
-        }
-        for (int f0 = 0; f0 < K; f0 += 8) {
-          float fx[8];
-          uint32_t fi[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            fx[u] = s_bx[kChunkCap + f0 + u];
-            fi[u] = s_bi[kChunkCap + f0 + u];
-          }
-#pragma unroll
-          for (int u = 0; u < 8; ++u) rank += (f0 + u < K && beats(fx[u], fi[u], xe, ie)) ? 1 : 0;
-        }
-        const int nvalid = __popcll(__ballot(valid_e));
-        if (valid_e && rank < K) s_order[rank] = lane;
-        wave_sync_lds();
-        const int nsel_s = min(nvalid, K);
-        src = lane < nsel_s ? s_order[lane] : 0;
-        x = __shfl(xe, src);
-        idx = __shfl(ie, src);
-        lmt = __shfl(lmt_e, src);
-        btk = __shfl(btk_e, src);
-        if (lane >= nsel_s) {
-          x = kNegInf;
-          idx = 0xFFFFFFFFu;
-        }
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-          hh[l].begin = __shfl(hh[l].begin, src);
-          hh[l].count = __shfl(hh[l].count, src);
-          hh[l].bo = __shfl(hh[l].bo, src);
-        }
-        if (HAS_BT) {
-          nd.list_begin = __shfl(nd.list_begin, src);
-          nd.list_count = __shfl(nd.list_count, src);
-          nd.pot = __shfl(nd.pot, src);
-          nd.chain_arcs = __shfl(nd.chain_arcs, src);
-        }
-      } else {
-        x = j < K ? s_nx[j] : kNegInf;
-        idx = j < K ? s_ni[j] : 0xFFFFFFFFu;
-        if (idx == 0xFFFFFFFFu) x = kNegInf;
-        lmt = j < K ? s_nlm[j] : 0u;
-        btk = j < K ? s_nbt[j] : 0u;
-        const bool valid = x != kNegInf;
-        const uint32_t vpar = valid ? idx / static_cast<uint32_t>(W) : 0u;
-        const int vc = valid ? static_cast<int>(idx - vpar * W) : V;
-        const bool vemit = valid && vc != V && vc != s_last[vpar];
-#pragma unroll
-        for (int l = 0; l < NL; ++l) hh[l] = p.lm_states[static_cast<size_t>(vemit ? lmt : p.lm_bos_state) * NL + l];
-        if (HAS_BT) nd = p.bt_nodes[vemit ? (btk & kBtChildMask) : 0u];
-      }
-      // prune (Algorithm 1: below best - theta -> -inf)
-      const float best = __shfl(x, 0);
-      const float lim = best - p.theta;
-      bool valid = (j < K) && (x != kNegInf);
-      if (valid && x < lim) x = kNegInf;
-      int32_t last = V, len = 0;
-      uint64_t hash = 0ull;
-      uint32_t lms = 0u, bts = 0u;
-      int32_t bpv = -1;
-      bool emit = false;
-      int par = 0;
+    // ---- U. prune, advance, recombine (every wave, lane j = slot j) ----
+    {
+      const int nsel = min(K, nfin);
+      const bool valid = j < nsel;
+      float x = kNegInf;
+      uint32_t idx = 0u, lmt = 0u, btk = 0u;
       if (valid) {
-        par = static_cast<int>(idx / static_cast<uint32_t>(W));
-        const int c = static_cast<int>(idx - static_cast<uint32_t>(par) * W);
-        const int lastp = s_last[par];
-        emit = (c != V) && (c != lastp);
-        hash = s_hash[par];
-        len = s_len[par];
-        lms = s_lms[par];
-        bts = s_bts[par];
-        if (emit) {
-          hash = mix_token(hash, static_cast<uint32_t>(c));
-          len += 1;
-          if (HAS_LM) lms = lmt;
-          if (HAS_BT) bts = btk & kBtChildMask;
-        }
-        last = c;
-        bpv = (par << 16) | c;
+        const uint4 e = s_res[mpar][j];
+        x = __uint_as_float(e.x);
+        idx = e.y;
+        lmt = e.z;
+        btk = e.w;
       }
-      if (x != kNegInf && emit) st_emit += 1;
-      // recombination: same transcript hash, length and ends-in-blank flag
-      bool alive = valid && (x != kNegInf);
-      const int blankend = (last == V) ? 1 : 0;
-      const uint32_t meta = (static_cast<uint32_t>(len) & 0x3FFFFFFFu) | (static_cast<uint32_t>(blankend) << 30) |
-                            (alive ? 0x80000000u : 0u);
-      if (j < K) {
-        s_rkh[j] = hash;
-        s_rkm[j] = meta;
+      const uint32_t par = valid ? idx / static_cast<uint32_t>(W) : 0u;
+      const int c = valid ? static_cast<int>(idx - par * static_cast<uint32_t>(W)) : V;
+      const int ipar = static_cast<int>(par);
+      // parent fields (every lane takes part in the exchange)
+      const int lastp = __shfl(last, ipar);
+      const uint64_t hashp = __shfl(hash, ipar);
+      const int lenp = __shfl(len, ipar);
+      const uint32_t lmsp = __shfl(lms, ipar), btsp = __shfl(bts, ipar);
+      uint32_t pb[NLA], pc[NLA];
+      float pbo[NLA];
+#pragma unroll
+      for (int l = 0; l < NL; ++l) {
+        pb[l] = __shfl(lvb[l], ipar);
+        pc[l] = __shfl(lvc[l], ipar);
+        pbo[l] = __shfl(lvbo[l], ipar);
       }
-      wave_sync_lds();
+      uint32_t pbb = 0u, pbc = 0u;
+      int32_t pbp = 0;
+      if (HAS_BT) {
+        pbb = __shfl(btb, ipar);
+        pbc = __shfl(btc, ipar);
+        pbp = __shfl(btpot, ipar);
+      }
+      const bool emit = valid && c != V && c != lastp;
+      // chain headers of emitting winners (issued early, used at the end)
+      LmLevel hh[NLA];
+#pragma unroll
+      for (int l = 0; l < NL; ++l) hh[l] = p.lm_states[static_cast<size_t>(emit ? lmt : p.lm_bos_state) * NL + l];
+      BtNode nd{0u, 0u, 0u, 0u};
+      if (HAS_BT) nd = p.bt_nodes[emit ? (btk & kBtChildMask) : 0u];
+      // prune (Algorithm 1: below best - theta -> -inf)
+      const float best = rdlane(x, 0);
+      const float lim = best - p.theta;
+      if (valid && x < lim) x = kNegInf;
+      const bool emit_fin = x != kNegInf && emit;
+      const int32_t nlast = valid ? c : V;
+      const int32_t nlen = valid ? lenp + (emit ? 1 : 0) : 0;
+      const uint64_t nhash = valid ? (emit ? mix_token(hashp, static_cast<uint32_t>(c)) : hashp) : 0ull;
+      const uint32_t nlms = valid ? ((HAS_LM && emit) ? lmt : lmsp) : 0u;
+      const uint32_t nbts = valid ? ((HAS_BT && emit) ? (btk & kBtChildMask) : btsp) : 0u;
+      // recombination: same transcript hash, length and ends-in-blank flag as
+      // a live lower slot
+      const bool alive0 = valid && x != kNegInf;
+      const uint32_t meta = (static_cast<uint32_t>(nlen) & 0x3FFFFFFFu) | ((nlast == V ? 1u : 0u) << 30);
+      const uint64_t amask0 = __ballot(alive0);
       bool dup = false;
-      for (int i0 = 0; i0 < K; i0 += 8) {
-        uint32_t mi[8];
-        uint64_t hi[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          mi[u] = s_rkm[i0 + u];
-          hi[u] = s_rkh[i0 + u];
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int i = i0 + u;
-          if (i < j && i < K && alive && (mi[u] >> 31) && hi[u] == hash && ((mi[u] ^ meta) & 0x7FFFFFFFu) == 0u)
-            dup = true;
+      {
+        uint64_t mr = amask0 & ~(1ull << 63);  // the top lane can never be the lower slot of a pair
+        while (mr) {
+          const int i = static_cast<int>(__builtin_ctzll(mr));
+          mr &= mr - 1ull;
+          const uint32_t hlo = rdlane(static_cast<uint32_t>(nhash), i);
+          const uint32_t hhi = rdlane(static_cast<uint32_t>(nhash >> 32), i);
+          const uint32_t mi = rdlane(meta, i);
+          dup = dup || (j > i && alive0 && static_cast<uint32_t>(nhash) == hlo &&
+                        static_cast<uint32_t>(nhash >> 32) == hhi && meta == mi);
         }
       }
       if (dup) x = kNegInf;
-      alive = alive && !dup;
-      // next chain: prefetched for emitting winners, the parent's otherwise
-      uint32_t cb[NLA], cc[NLA];
-      float cbo[NLA];
-      uint32_t bb = 0u, bc = 0u;
-      int32_t bpot = 0;
-      if (alive) {
+      const bool nalive = alive0 && !dup;
+      if (wave == 0 && j < K)
+        bpb[static_cast<size_t>(t) * K + j] = valid ? static_cast<int32_t>((par << 16) | static_cast<uint32_t>(c)) : -1;
+      // new state
+      sc = x;
+      last = nlast;
+      len = nlen;
+      hash = nhash;
+      lms = nlms;
+      bts = nbts;
+      alive = nalive;
+      int32_t acnt = 0;
 #pragma unroll
-        for (int l = 0; l < NL; ++l) {
-          cb[l] = emit ? hh[l].begin : s_lvb[par][l];
-          cc[l] = emit ? hh[l].count : s_lvc[par][l];
-          cbo[l] = emit ? hh[l].bo : s_lvbo[par][l];
-        }
-        if (HAS_BT) {
-          bb = emit ? nd.list_begin : s_btb[par];
-          bc = emit ? nd.list_count : s_btc[par];
-          bpot = emit ? static_cast<int32_t>(nd.pot & 0xFFu) : s_btpot[par];
-        }
+      for (int l = 0; l < NL; ++l) {
+        lvb[l] = nalive ? (emit ? hh[l].begin : pb[l]) : 0u;
+        lvc[l] = nalive ? (emit ? hh[l].count : pc[l]) : 0u;
+        lvbo[l] = nalive ? (emit ? hh[l].bo : pbo[l]) : 0.0f;
+        acnt += static_cast<int32_t>(lvc[l] & ~kExists);
       }
-      uint32_t chain_nodes = 0u, chain_arcs = 0u;
-      if (HAS_BT && alive) {
-        // statistics: the parent's record when not emitting
-        if (emit) {
-          chain_nodes = nd.pot >> 8;
-          chain_arcs = nd.chain_arcs;
-        }
+      if (HAS_BT) {
+        btb = nalive ? (emit ? nd.list_begin : pbb) : 0u;
+        btc = nalive ? (emit ? nd.list_count : pbc) : 0u;
+        btpot = nalive ? (emit ? static_cast<int32_t>(nd.pot & 0xFFu) : pbp) : 0;
       }
-      wave_sync_lds();  // every lane has read the parents' rows and the survivors
-      // reset the survivor buffer for the next frame (visible after the barrier)
-      if (lane == 0) {
-        s_nbuf = 0;
-        s_overflow = 0;
-      }
-      if (j < K) {
-        s_bx[kChunkCap + j] = kNegInf;
-        s_bi[kChunkCap + j] = 0xFFFFFFFFu;
-      }
-      int32_t acnt = 0, bcnt = 0;
-      if (j < K) {
-        bpb[static_cast<size_t>(t) * K + j] = bpv;
-        s_score[j] = x;
-        s_last[j] = last;
-        s_len[j] = len;
-        s_hash[j] = hash;
-        s_lms[j] = lms;
-        s_bts[j] = bts;
-      }
-      if (alive) {
+      if (want_stats && wave == 0) {
+        // chain work of the next frame (alive beams) and this frame's
+        // emitting winners
+        uint32_t s_ls = 0u, s_la = 0u, s_bn = 0u, s_ba = 0u;
+        const bool counted = t + 1 < L && nalive;
+        if (counted) {
 #pragma unroll
-        for (int l = 0; l < NL; ++l) {
-          s_lvb[j][l] = cb[l];
-          s_lvc[j][l] = cc[l];
-          s_lvbo[j][l] = cbo[l];
-          const uint32_t n = cc[l] & ~kExists;
-          acnt += static_cast<int32_t>(n);
-          if (t + 1 < L && (cc[l] & kExists)) {
-            st_lms += 1;
-            st_lma += n;
+          for (int l = 0; l < NL; ++l) {
+            if (lvc[l] & kExists) {
+              s_ls += 1u;
+              s_la += lvc[l] & ~kExists;
+            }
           }
+          if (HAS_BT) {
+            // boosting statistics need the node record of inherited states too
+            const BtNode pn = emit ? nd : p.bt_nodes[bts];
+            s_bn = pn.pot >> 8;
+            s_ba = pn.chain_arcs;
+          }
+          atomicAdd(&s_st[0], 1ull);
         }
-        if (HAS_BT) {
-          s_btb[j] = bb;
-          s_btc[j] = bc;
-          s_btpot[j] = bpot;
-          bcnt = static_cast<int32_t>(bc);
-        }
-        if (t + 1 < L) st_alive += 1;
+        if (s_ls) atomicAdd(&s_st[1], static_cast<unsigned long long>(s_ls));
+        if (s_la) atomicAdd(&s_st[2], static_cast<unsigned long long>(s_la));
+        if (s_bn) atomicAdd(&s_st[3], static_cast<unsigned long long>(s_bn));
+        if (s_ba) atomicAdd(&s_st[4], static_cast<unsigned long long>(s_ba));
+        if (emit_fin) atomicAdd(&s_st[5], 1ull);
       }
-      // boosting statistics need the node record of inherited states too
-      if (HAS_BT && alive && !emit && t + 1 < L && p.stats) {
-        const BtNode pn = p.bt_nodes[bts];
-        chain_nodes = pn.pot >> 8;
-        chain_arcs = pn.chain_arcs;
-      }
-      if (t + 1 < L) {
-        st_btn += chain_nodes;
-        st_bta += chain_arcs;
-      }
-      // live list and chunking (slot order = live order)
-      const uint64_t amask = __ballot(alive);
+      // live positions and beam records for the next frame
+      const uint64_t amask = __ballot(nalive);
       const int na = __popcll(amask);
-      const int apos = __popcll(amask & lanemask_lt());
-      const int av = alive ? acnt : 0, bv = alive ? bcnt : 0;
-      const int ia_slot = wave_incl_scan(av, lane);
-      const int ib_slot = wave_incl_scan(bv, lane);
-      if (alive) {
-        s_alive[apos] = j;
-        s_hoff[apos] = ia_slot - av;
-        s_boff[apos] = ib_slot - bv;
-      }
-      const int tota = __builtin_amdgcn_readlane(ia_slot, 63);
-      const int totb = __builtin_amdgcn_readlane(ib_slot, 63);
-      if (lane == 0) {
-        s_hoff[na] = tota;
-        s_boff[na] = totb;
-      }
-      int nch = 0;
-      if (na <= kcmax && tota <= kLmStage && totb <= kBtStage) {
-        if (lane == 0) s_chunk[0] = 0;
+      const int lp = __popcll(amask & lmlt);
+      if (wave == 0 && nalive) put_row(lp);
+      // chunk plan: live slots in slot order, at most kcmax beams and
+      // kLmStage staged arcs per chunk
+      const int ia = wave_incl_scan(acnt, lane);
+      const int tota = rdlane(ia, 63);
+      if (na <= kcmax && tota <= kLmStage) {
         nch = na > 0 ? 1 : 0;
+        cid = 0;
       } else {
-        wave_sync_lds();
-        // inclusive sums by live position
-        const int ia = lane < na ? s_hoff[lane + 1] : tota;
-        const int ib = lane < na ? s_boff[lane + 1] : totb;
+        nch = 0;
+        cid = -1;
         int start = 0;
         while (start < na) {
-          const int basea = start > 0 ? __shfl(ia, start - 1) : 0;
-          const int baseb = start > 0 ? __shfl(ib, start - 1) : 0;
-          const bool ok = lane >= start && lane < na && lane < start + kcmax &&
-                          (ia - basea) <= kLmStage && (ib - baseb) <= kBtStage;
+          const uint64_t sm = __ballot(nalive && lp == start);
+          const int sl = static_cast<int>(__builtin_ctzll(sm));
+          const int basea = rdlane(ia - acnt, sl);
+          const bool ok = nalive && lp >= start && lp < start + kcmax && (ia - basea) <= kLmStage;
           int cnt = __popcll(__ballot(ok));
           if (cnt == 0) {
-            cnt = 1;
+            cnt = 1;  // a single chain above the staging limit (the builders prevent it)
             status |= 4u;
           }
-          if (lane == 0) s_chunk[nch] = start;
+          if (nalive && lp >= start && lp < start + cnt) cid = nch;
           ++nch;
           start += cnt;
         }
       }
-      if (lane == 0) {
-        s_chunk[nch] = na;
-        s_nchunk = nch;
-      }
     }
-    __syncthreads();
   }
 
   // ---- LM.Final, best beam ----
   if (wave == 0) {
-    const int j = lane;
-    float s = (j < K) ? s_score[j] : kNegInf;
+    float s = sc;
     if (HAS_LM && j < K && s != kNegInf) {
       // ln P(</s> | state) through the backoff chain; </s> is the last arc of
       // a state's sorted arcs when present
@@ -1056,9 +1009,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       float fv = 0.0f;
 #pragma unroll
       for (int l = NL - 1; l >= 0; --l) {
-        const uint32_t n = s_lvc[j][l] & ~kExists;
+        const uint32_t n = lvc[l] & ~kExists;
         if (found < 0 && n > 0) {
-          const LmArc a = p.lm_arcs[s_lvb[j][l] + n - 1];
+          const LmArc a = p.lm_arcs[lvb[l] + n - 1];
           if (a.token == static_cast<uint32_t>(V)) {
             found = l;
             fv = a.logp;
@@ -1069,16 +1022,16 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         v = fv;
 #pragma unroll
         for (int l = 0; l < NL; ++l)
-          if (l > found) v = v + s_lvbo[j][l];
+          if (l > found) v = v + lvbo[l];
       } else {
 #pragma unroll
-        for (int l = 0; l < NL; ++l) v = v + s_lvbo[j][l];
+        for (int l = 0; l < NL; ++l) v = v + lvbo[l];
       }
       const float av = alpha * v;
       s = s + av;
     }
     // argmax, lowest slot on ties
-    float bs = s;
+    float bs = (j < K) ? s : kNegInf;
     int bj = (j < K) ? j : 0x7FFF;
     for (int off = 1; off < 64; off <<= 1) {
       const float os = __shfl_xor(bs, off);
@@ -1088,40 +1041,29 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         bj = oj;
       }
     }
+    const int blen = __shfl(len, bj < 64 ? bj : 0);
     if (lane == 0) {
       s_best = bj;
       s_bestscore = bs;
+      s_bestlen = blen;
     }
-    if (p.stats) {
-      int64_t a0 = st_alive, a1 = st_lms, a2 = st_lma, a3 = st_btn, a4 = st_bta, a5 = st_emit;
-      for (int off = 1; off < 64; off <<= 1) {
-        a0 += __shfl_xor(a0, off);
-        a1 += __shfl_xor(a1, off);
-        a2 += __shfl_xor(a2, off);
-        a3 += __shfl_xor(a3, off);
-        a4 += __shfl_xor(a4, off);
-        a5 += __shfl_xor(a5, off);
-      }
-      if (lane == 0) {
-        int64_t* so = p.stats + static_cast<size_t>(b) * 8;
-        so[0] = L;
-        so[1] = a0;
-        so[2] = a1;
-        so[3] = a2;
-        so[4] = a3;
-        so[5] = a4;
-        so[6] = a5;
-        so[7] = 0;
-      }
+    if (want_stats && lane == 0) {
+      // wave 0 made every update of s_st (LDS operations of one wave complete
+      // in order)
+      int64_t* so = p.stats + static_cast<size_t>(b) * 8;
+      so[0] = L;
+#pragma unroll
+      for (int q = 0; q < 6; ++q) so[1 + q] = static_cast<int64_t>(s_st[q]);
+      so[7] = 0;
     }
   }
   __syncthreads();
   const int best = s_best;
   const float bscore = s_bestscore;
   const bool have = bscore != kNegInf;
-  const int nout = have ? s_len[best] : 0;
+  const int nout = have ? s_bestlen : 0;
   int32_t* ot = p.out_tokens + static_cast<size_t>(b) * T;
-  for (int t = nout + tid; t < T; t += kThreads) ot[t] = -1;
+  for (int tt = nout + tid; tt < T; tt += kThreads) ot[tt] = -1;
   if (tid == 0) {
     p.out_scores[b] = bscore;
     if (p.out_lengths) p.out_lengths[b] = nout;
@@ -1130,7 +1072,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // ---- traceback through the back-pointers, staged in LDS tiles ----
   if (have && L > 0) {
     const int tile_frames = kBigWords / K;
-    int j = best, cnext = -1, pos = nout;
+    int jb = best, cnext = -1, pos = nout;
     for (int hi = L; hi > 0;) {
       const int lo = hi > tile_frames ? hi - tile_frames : 0;
       __syncthreads();
@@ -1139,15 +1081,15 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       for (int q = tid; q < n; q += kThreads) s_big[q] = static_cast<uint32_t>(src[q]);
       __syncthreads();
       if (tid == 0) {
-        for (int t = hi - 1; t >= lo; --t) {
-          const uint32_t e = s_big[(t - lo) * K + j];
-          const int c = static_cast<int>(e & 0xFFFFu);
+        for (int tt = hi - 1; tt >= lo; --tt) {
+          const uint32_t e = s_big[(tt - lo) * K + jb];
+          const int cl = static_cast<int>(e & 0xFFFFu);
           const int par = static_cast<int>(e >> 16);
-          if (t < L - 1 && cnext != V && cnext != c) {
+          if (tt < L - 1 && cnext != V && cnext != cl) {
             if (pos > 0) ot[--pos] = cnext;
           }
-          cnext = c;
-          j = par;
+          cnext = cl;
+          jb = par;
         }
       }
       hi = lo;

@@ -421,10 +421,8 @@ int build_boost_tables(int V, int n_phrases, const int32_t* offsets, const int32
         bt->list.push_back(BtEntry{static_cast<uint32_t>(kc.first), k});
       }
     }
+    // tokens are unique within a merged list, so cnt <= V
     const uint32_t cnt = static_cast<uint32_t>(bt->list.size()) - begin;
-    if (cnt > static_cast<uint32_t>(ctcbeam::kBtStage))
-      return fail(2, "a boosting tree state has more than " + std::to_string(ctcbeam::kBtStage) +
-                         " continuations on its failure chain");
     bt->nodes[q] = BtNode{begin, cnt, static_cast<uint32_t>(pot[q]) | (chain_nodes << 8), chain_arcs};
   }
   bt->root_key.assign(V, 0u);

@@ -10,10 +10,9 @@ constexpr int kThreads = 512;         // threads per workgroup (8 wave64)
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxK = 64;             // beam size limit
 constexpr int kMaxLev = 7;            // LM order - 1 limit
-constexpr int kKeyWords = 8192;       // per-chunk [hyp][token] key rows (u32 each)
-constexpr int kLmStage = 4096;        // staged LM arcs per chunk
-constexpr int kBtStage = 2048;        // staged boosting continuations per chunk
-constexpr int kCap = 512;             // candidate buffer entries
+constexpr int kKeyWords = 8192;       // per-chunk [hyp][token] key row entries
+constexpr int kLmStage = 4096;        // staged LM arcs per chunk (12-bit slot)
+constexpr int kCap = 512;             // survivor pool entries
 constexpr uint32_t kExists = 0x80000000u;
 
 // LM state record, one per chain level l (context of length l+1):
