@@ -234,6 +234,20 @@ __device__ __forceinline__ float bitonic_levels(float v, int lane) {
   if constexpr (k < N) v = bitonic_levels<N, k * 2>(v, lane);
   return v;
 }
+// Recombination probe at distance D = 1..15 (lane j against lane j-D of its
+// 16-lane row), for the D below the beam size.
+template <int D>
+__device__ __forceinline__ void recomb_shifts(int K, uint32_t hlo, uint32_t hhi, uint32_t mkey, bool& dup) {
+  if (D < K) {  // wave-uniform
+    constexpr int kCtrl = 0x110 + D;  // row_shr:D
+    const uint32_t ol = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(hlo), kCtrl, 0xF, 0xF, false));
+    const uint32_t oh = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(hhi), kCtrl, 0xF, 0xF, false));
+    const uint32_t om = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(mkey), kCtrl, 0xF, 0xF, false));
+    dup = dup || (ol == hlo && oh == hhi && om == mkey);
+    if constexpr (D < 15) recomb_shifts<D + 1>(K, hlo, hhi, mkey, dup);
+  }
+}
+
 // Bitonic sort of one value per lane within groups of N lanes, descending.
 template <int N>
 __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
@@ -251,6 +265,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // a chunk has at most 64 LM segments (beam, level): one lane each
   constexpr int KSEG = (NL > 0 && KCR * NL > 64) ? 64 / (NL > 0 ? NL : 1) : KCR;
   constexpr int kRowWords = 16;               // beam record per live position
+  // beam state record (one per slot, double-buffered by frame): score bits,
+  // back-pointer, transcript hash (2), length, last label, LM state, boosting
+  // state, emitted flag, boosting list begin/count/pot, LM chain begin[NL],
+  // count[NL], backoff[NL]
+  constexpr int kRX = 0, kRBp = 1, kRHlo = 2, kRHhi = 3, kRLen = 4, kRLast = 5, kRLms = 6, kRBts = 7;
+  constexpr int kREmit = 8, kRBtb = 9, kRBtc = 10, kRBtp = 11, kRLvb = 12, kRLvc = 12 + NL, kRLvbo = 12 + 2 * NL;
+  constexpr int RW = (12 + 3 * NL + 3) & ~3;
 
   __shared__ __align__(16) uint32_t s_big[kBigWords];
   // survivor pool: score bits, flat index, LM target (raw), boosting key
@@ -259,6 +280,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   __shared__ uint4 s_res[2][kMaxK];
   // beam records by live position: score, last label, slot, pot, backoff weights
   __shared__ __align__(16) uint32_t s_row[(kMaxK + 16) * kRowWords];
+  // beam state records by slot: [rcur] the current beam, [rcur ^ 1] its successors
+  __shared__ __align__(16) uint32_t s_rec[2 * kMaxK * RW];
   __shared__ float s_top[kWaves * 8];
   __shared__ uint64_t s_red[2][kWaves];
   __shared__ int32_t s_nbuf, s_overflow;
@@ -313,8 +336,6 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   const int j = lane;
   float sc = (j == 0) ? 0.0f : kNegInf;
   int32_t last = V, len = 0;
-  uint64_t hash = 0ull;
-  uint32_t lms = HAS_LM ? p.lm_bos_state : 0u, bts = 0u;
   uint32_t lvb[NLA], lvc[NLA];
   float lvbo[NLA];
 #pragma unroll
@@ -358,12 +379,98 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // chunk plan: chunk id of each live slot, number of chunks (uniform)
   int cid = 0;
   int nch = 1;
+  int rcur = 0;  // s_rec buffer holding the current beam
+  // record helpers
+  auto load_rec = [&](const uint32_t* src, uint32_t (&r)[RW]) {
+#pragma unroll
+    for (int w4 = 0; w4 < RW; w4 += 4) {
+      const uint4 v = *reinterpret_cast<const uint4*>(src + w4);
+      r[w4] = v.x;
+      r[w4 + 1] = v.y;
+      r[w4 + 2] = v.z;
+      r[w4 + 3] = v.w;
+    }
+  };
+  auto store_rec = [&](uint32_t* dst, const uint32_t (&r)[RW]) {
+#pragma unroll
+    for (int w4 = 0; w4 < RW; w4 += 4) *reinterpret_cast<uint4*>(dst + w4) = make_uint4(r[w4], r[w4 + 1], r[w4 + 2], r[w4 + 3]);
+  };
+  // successor of a selected candidate (flat index idx, resolved LM target,
+  // boosting key) from its parent's record: first the parent, the emitted
+  // flag and the chain headers of an emitted token (global loads in flight),
+  // then the record
+  struct Succ {
+    uint32_t par, lmt, btk;
+    int c;
+    bool emit;
+    LmLevel hh[NLA];
+    BtNode nd;
+  };
+  auto succ_begin = [&](bool act, uint32_t idx, uint32_t lmt, uint32_t btk, const uint32_t* prec, Succ& sp) {
+    sp.par = act ? idx / static_cast<uint32_t>(W) : 0u;
+    sp.c = act ? static_cast<int>(idx - sp.par * static_cast<uint32_t>(W)) : V;
+    sp.lmt = lmt;
+    sp.btk = btk;
+    const int lastp = static_cast<int>(prec[sp.par * RW + kRLast]);
+    sp.emit = act && sp.c != V && sp.c != lastp;
+#pragma unroll
+    for (int l = 0; l < NL; ++l)
+      sp.hh[l] = p.lm_states[static_cast<size_t>(sp.emit ? lmt : p.lm_bos_state) * NL + l];
+    sp.nd = BtNode{0u, 0u, 0u, 0u};
+    if (HAS_BT) sp.nd = p.bt_nodes[sp.emit ? (btk & kBtChildMask) : 0u];
+  };
+  auto succ_end = [&](const Succ& sp, uint32_t xbits, const uint32_t* prec, uint32_t* dst) {
+    uint32_t r[RW];
+    load_rec(prec + sp.par * RW, r);
+    const bool e = sp.emit;
+    uint64_t h = (static_cast<uint64_t>(r[kRHhi]) << 32) | r[kRHlo];
+    if (e) h = mix_token(h, static_cast<uint32_t>(sp.c));
+    r[kRX] = xbits;
+    r[kRBp] = (sp.par << 16) | static_cast<uint32_t>(sp.c);
+    r[kRHlo] = static_cast<uint32_t>(h);
+    r[kRHhi] = static_cast<uint32_t>(h >> 32);
+    r[kRLen] += e ? 1u : 0u;
+    r[kRLast] = static_cast<uint32_t>(sp.c);
+    if (HAS_LM && e) r[kRLms] = sp.lmt;
+    if (HAS_BT && e) r[kRBts] = sp.btk & kBtChildMask;
+    r[kREmit] = e ? 1u : 0u;
+    if (HAS_BT && e) {
+      r[kRBtb] = sp.nd.list_begin;
+      r[kRBtc] = sp.nd.list_count;
+      r[kRBtp] = sp.nd.pot & 0xFFu;
+    }
+#pragma unroll
+    for (int l = 0; l < NL; ++l) {
+      if (e) {
+        r[kRLvb + l] = sp.hh[l].begin;
+        r[kRLvc + l] = sp.hh[l].count;
+        r[kRLvbo + l] = __float_as_uint(sp.hh[l].bo);
+      }
+    }
+    store_rec(dst, r);
+  };
 
   for (int i = tid; i < kOffTgt; i += kThreads) s_big[i] = 0u;
   for (int i = tid; i < (kMaxK + 16) * kRowWords; i += kThreads) s_row[i] = 0u;
   __syncthreads();
   if (tid == 0) {
     put_row(0);
+    // record of the initial beam (slot 0)
+    uint32_t r[RW];
+#pragma unroll
+    for (int w = 0; w < RW; ++w) r[w] = 0u;
+    r[kRLast] = static_cast<uint32_t>(V);
+    r[kRLms] = HAS_LM ? p.lm_bos_state : 0u;
+    r[kRBtb] = btb;
+    r[kRBtc] = btc;
+    r[kRBtp] = static_cast<uint32_t>(btpot);
+#pragma unroll
+    for (int l = 0; l < NL; ++l) {
+      r[kRLvb + l] = lvb[l];
+      r[kRLvc + l] = lvc[l];
+      r[kRLvbo + l] = __float_as_uint(lvbo[l]);
+    }
+    store_rec(s_rec, r);
     s_nbuf = 0;
     s_overflow = 0;
     if (want_stats) {
@@ -463,50 +570,40 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             S += nl;
           }
         }
+        // tiles of 64 arcs never straddle segments: a tile's segment is one
+        // ballot away and its fields are wave-uniform (readlane)
         const int sincl = wave_incl_scan(static_cast<int>(sg_cnt), lane);
-        const uint32_t sstart = static_cast<uint32_t>(sincl) - sg_cnt;
-        const uint32_t ntot = static_cast<uint32_t>(rdlane(sincl, 63));
-        const uint32_t sg_off = sg_base - sstart;  // arc index = sg_off + position
-        const bool sg_live = lane < S;
-        const int ntile = static_cast<int>((ntot + 63u) >> 6);
+        const uint32_t sstart = static_cast<uint32_t>(sincl) - sg_cnt;  // staging slot of the first arc
+        const int stl = static_cast<int>((sg_cnt + 63u) >> 6);
+        const int tincl = wave_incl_scan(stl, lane);
+        const int texcl = tincl - stl;
+        const int ntile = rdlane(tincl, 63);
         for (int t0 = wave; t0 < ntile; t0 += kWaves * kTileUnroll) {
           LmArc a[kTileUnroll];
-          uint32_t arl[kTileUnroll];
+          uint32_t apos[kTileUnroll], arl[kTileUnroll];
           float af[kTileUnroll][NF];
 #pragma unroll
           for (int u = 0; u < kTileUnroll; ++u) {
             const int tt = t0 + u * kWaves;
+            apos[u] = 0xFFFFFFFFu;
             arl[u] = 0u;
             a[u].token = 0xFFFFFFFFu;
             if (tt < ntile) {  // wave-uniform
-              // tile = 64 consecutive positions; the segment of lane 0 plus
-              // the segments starting inside the tile give each lane's
-              const uint32_t q0 = static_cast<uint32_t>(tt) << 6;
-              const int s0 = __popcll(__ballot(sg_live && sstart <= q0)) - 1;
-              uint64_t bm = __ballot(sg_live && sstart > q0 && sstart < q0 + 64u);
-              uint64_t om = 0ull;
-              while (bm) {
-                const int sb = static_cast<int>(__builtin_ctzll(bm));
-                bm &= bm - 1ull;
-                om |= 1ull << (rdlane(sstart, sb) - q0);
-              }
-              const int seg = s0 + __popc(static_cast<uint32_t>(om) & lmle_lo) +
-                              __popc(static_cast<uint32_t>(om >> 32) & lmle_hi);
-              const int sa = seg << 2;
-              const uint32_t q = q0 + static_cast<uint32_t>(lane);
-              const uint32_t off = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(sa, static_cast<int>(sg_off)));
-              arl[u] = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(sa, static_cast<int>(sg_rl)));
+              const int sg = __popcll(__ballot(tincl <= tt));
+              const uint32_t qs = (static_cast<uint32_t>(tt - rdlane(texcl, sg)) << 6) + static_cast<uint32_t>(lane);
+              const bool ok = qs < rdlane(sg_cnt, sg);
+              apos[u] = ok ? rdlane(sstart, sg) + qs : 0xFFFFFFFFu;
+              arl[u] = rdlane(sg_rl, sg);
 #pragma unroll
-              for (int k = 0; k + 1 < NL; ++k)
-                af[u][k] = __int_as_float(__builtin_amdgcn_ds_bpermute(sa, __float_as_int(sg_f[k])));
-              a[u] = p.lm_arcs[q < ntot ? off + q : 0u];
+              for (int k = 0; k + 1 < NL; ++k) af[u][k] = rdlane(sg_f[k], sg);
+              a[u] = p.lm_arcs[rdlane(sg_base, sg) + (ok ? qs : 0u)];
             }
           }
 #pragma unroll
           for (int u = 0; u < kTileUnroll; ++u) {
-            const uint32_t q = (static_cast<uint32_t>(t0 + u * kWaves) << 6) + static_cast<uint32_t>(lane);
-            // positions past the chunk's arcs (and tiles past the last) skip
-            if (q < ntot && a[u].token < static_cast<uint32_t>(V)) {
+            const uint32_t q = apos[u];
+            // positions past a segment's arcs (and tiles past the last) skip
+            if (q != 0xFFFFFFFFu && a[u].token < static_cast<uint32_t>(V)) {
               float v = a[u].logp;
 #pragma unroll
               for (int k = 0; k + 1 < NL; ++k) v = v + af[u][k];
@@ -529,45 +626,33 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const int addr = dst << 2;
           uint32_t bg_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(nb)));
           const uint32_t bg_base = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(btb)));
-          const uint32_t bg_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, row));
-          const bool bg_live = lane < S;
-          if (!bg_live) bg_cnt = 0u;
-          const int bincl = wave_incl_scan(static_cast<int>(bg_cnt), lane);
-          const uint32_t bstart = static_cast<uint32_t>(bincl) - bg_cnt;
-          const uint32_t nbt = static_cast<uint32_t>(rdlane(bincl, 63));
-          const uint32_t bg_off = bg_base - bstart;
-          const int ntile = static_cast<int>((nbt + 63u) >> 6);
+          const uint32_t bg_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(row)));
+          if (lane >= S) bg_cnt = 0u;
+          const int btl = static_cast<int>((bg_cnt + 63u) >> 6);
+          const int tincl = wave_incl_scan(btl, lane);
+          const int texcl = tincl - btl;
+          const int ntile = rdlane(tincl, 63);
           for (int t0 = wave; t0 < ntile; t0 += kWaves * kTileUnroll) {
             BtEntry e[kTileUnroll];
             uint32_t erow[kTileUnroll];
+            bool eok[kTileUnroll];
 #pragma unroll
             for (int u = 0; u < kTileUnroll; ++u) {
               const int tt = t0 + u * kWaves;
               erow[u] = 0u;
+              eok[u] = false;
               e[u].token = 0xFFFFFFFFu;
               if (tt < ntile) {  // wave-uniform
-                const uint32_t q0 = static_cast<uint32_t>(tt) << 6;
-                const int s0 = __popcll(__ballot(bg_live && bstart <= q0)) - 1;
-                uint64_t bm = __ballot(bg_live && bstart > q0 && bstart < q0 + 64u);
-                uint64_t om = 0ull;
-                while (bm) {
-                  const int sb = static_cast<int>(__builtin_ctzll(bm));
-                  bm &= bm - 1ull;
-                  om |= 1ull << (rdlane(bstart, sb) - q0);
-                }
-                const int seg = s0 + __popc(static_cast<uint32_t>(om) & lmle_lo) +
-                                __popc(static_cast<uint32_t>(om >> 32) & lmle_hi);
-                const int sa = seg << 2;
-                const uint32_t q = q0 + static_cast<uint32_t>(lane);
-                const uint32_t off = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(sa, static_cast<int>(bg_off)));
-                erow[u] = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(sa, static_cast<int>(bg_row)));
-                e[u] = p.bt_list[q < nbt ? off + q : 0u];
+                const int sg = __popcll(__ballot(tincl <= tt));
+                const uint32_t qs = (static_cast<uint32_t>(tt - rdlane(texcl, sg)) << 6) + static_cast<uint32_t>(lane);
+                eok[u] = qs < rdlane(bg_cnt, sg);
+                erow[u] = rdlane(bg_row, sg);
+                e[u] = p.bt_list[rdlane(bg_base, sg) + (eok[u] ? qs : 0u)];
               }
             }
 #pragma unroll
             for (int u = 0; u < kTileUnroll; ++u)
-              if (((static_cast<uint32_t>(t0 + u * kWaves) << 6) + static_cast<uint32_t>(lane)) < nbt &&
-                  e[u].token < static_cast<uint32_t>(V))
+              if (eok[u] && e[u].token < static_cast<uint32_t>(V))
                 btrow[erow[u] * V + e[u].token] = (e[u].key & kLowMask) | genhi;
           }
         }
@@ -705,18 +790,28 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       __syncthreads();  // C: pool complete
 
       // ---- R. exact rank of the pool: reserved region P + survivors ----
+      // The best K go to region Q in rank order; after the last chunk the
+      // winners' successor records go to s_rec[rcur ^ 1] instead.
       {
         const int P = mpar, Q = mpar ^ 1;
+        const bool last_chunk = ch + 1 == nch;
+        const uint32_t* prec = s_rec + rcur * (kMaxK * RW);
+        uint32_t* nrec = s_rec + (rcur ^ 1) * (kMaxK * RW);
         if (!s_overflow) {
           const int n = min(s_nbuf, kCap);
           const int N = K + n;
           nfin = 0;
           if (N <= 64) {
-            // one entry per lane; this wave ranks entries wave + 8u
+            // one entry per lane; this wave ranks (owns) entries wave + 8u
             uint4 eq = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
             if (lane < N) eq = (lane < K) ? s_res[P][lane] : s_pool[lane - K];
             const float xq = __uint_as_float(eq.x);
             nfin = __popcll(__ballot(xq != kNegInf));
+            const bool own = ((lane & (kWaves - 1)) == wave) && xq != kNegInf;
+            uint32_t lmt = eq.z;
+            if (HAS_LM && lane >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+            Succ sp;
+            if (last_chunk) succ_begin(own, eq.y, lmt, eq.w, prec, sp);  // loads overlap the ranking
             int myrank = K;
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
@@ -726,51 +821,58 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               const int rk = __popcll(__ballot(xq > xs || (xq == xs && eq.y < is)));
               myrank = ((lane >> 3) == u) ? rk : myrank;
             }
-            if ((lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf) {
-              uint32_t lmt = eq.z;
-              if (HAS_LM && lane >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
-              s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
+            if (own && myrank < K) {
+              if (last_chunk)
+                succ_end(sp, eq.x, prec, nrec + myrank * RW);
+              else
+                s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
             }
-          } else
-          // blocks of 64 entries: this wave ranks entries qb + (wave + 8u)
-          // against every entry, lane f holding entry fb + f
-          for (int qb = 0; qb < N; qb += 64) {
-            const int q = qb + lane;
-            uint4 eq = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
-            if (q < N) eq = (q < K) ? s_res[P][q] : s_pool[q - K];
-            const float xq = __uint_as_float(eq.x);
-            nfin += __popcll(__ballot(xq != kNegInf));
-            int rk[8];
+          } else {
+            // blocks of 64 entries: this wave ranks entries qb + (wave + 8u)
+            // against every entry, lane f holding entry fb + f
+            for (int qb = 0; qb < N; qb += 64) {
+              const int q = qb + lane;
+              uint4 eq = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+              if (q < N) eq = (q < K) ? s_res[P][q] : s_pool[q - K];
+              const float xq = __uint_as_float(eq.x);
+              nfin += __popcll(__ballot(xq != kNegInf));
+              int rk[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) rk[u] = 0;
-            for (int fb = 0; fb < N; fb += 64) {
-              float xf = xq;
-              uint32_t iff = eq.y;
-              if (fb != qb) {
-                const int f = fb + lane;
-                uint4 ef = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
-                if (f < N) ef = (f < K) ? s_res[P][f] : s_pool[f - K];
-                xf = __uint_as_float(ef.x);
-                iff = ef.y;
-              }
+              for (int u = 0; u < 8; ++u) rk[u] = 0;
+              for (int fb = 0; fb < N; fb += 64) {
+                float xf = xq;
+                uint32_t iff = eq.y;
+                if (fb != qb) {
+                  const int f = fb + lane;
+                  uint4 ef = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+                  if (f < N) ef = (f < K) ? s_res[P][f] : s_pool[f - K];
+                  xf = __uint_as_float(ef.x);
+                  iff = ef.y;
+                }
 #pragma unroll
-              for (int u = 0; u < 8; ++u) {
-                const int ql = wave + u * kWaves;
-                if (qb + ql < N) {  // wave-uniform
-                  const float xs = rdlane(xq, ql);
-                  const uint32_t is = rdlane(eq.y, ql);
-                  rk[u] += __popcll(__ballot(xf > xs || (xf == xs && iff < is)));
+                for (int u = 0; u < 8; ++u) {
+                  const int ql = wave + u * kWaves;
+                  if (qb + ql < N) {  // wave-uniform
+                    const float xs = rdlane(xq, ql);
+                    const uint32_t is = rdlane(eq.y, ql);
+                    rk[u] += __popcll(__ballot(xf > xs || (xf == xs && iff < is)));
+                  }
                 }
               }
-            }
-            // owner lane wave + 8u takes rank u
-            int myrank = K;
+              // owner lane wave + 8u takes rank u
+              int myrank = K;
 #pragma unroll
-            for (int u = 0; u < 8; ++u) myrank = ((lane >> 3) == u) ? rk[u] : myrank;
-            if ((lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf) {
+              for (int u = 0; u < 8; ++u) myrank = ((lane >> 3) == u) ? rk[u] : myrank;
+              const bool win = (lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf;
               uint32_t lmt = eq.z;
-              if (HAS_LM && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
-              s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
+              if (HAS_LM && win && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+              if (last_chunk) {
+                Succ sp;
+                succ_begin(win, eq.y, lmt, eq.w, prec, sp);
+                if (win) succ_end(sp, eq.x, prec, nrec + myrank * RW);
+              } else if (win) {
+                s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
+              }
             }
           }
         } else {
@@ -831,111 +933,87 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             ++nk;
           }
           nfin = nk;
+          if (last_chunk) {
+            __syncthreads();  // region Q complete
+            const bool act = wave == 0 && lane < nk;
+            uint4 e = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+            if (act) e = s_res[Q][lane];
+            Succ sp;
+            succ_begin(act, e.y, e.z, e.w, prec, sp);
+            if (act) succ_end(sp, e.x, prec, nrec + lane * RW);
+          }
         }
         // ranks [nfin, K) hold no candidate (the next chunk reads all K)
-        if (wave == 0 && lane >= nfin && lane < K) s_res[Q][lane] = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+        if (!last_chunk && wave == 0 && lane >= nfin && lane < K)
+          s_res[Q][lane] = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
       }
       __syncthreads();  // D: best K of the chunk in region Q
       mpar ^= 1;
-      if (nfin >= K) tau_run = fmaxf(tau_run, __uint_as_float(s_res[mpar][K - 1].x));
+      if (ch + 1 < nch && nfin >= K) tau_run = fmaxf(tau_run, __uint_as_float(s_res[mpar][K - 1].x));
       cs += kc;
     }
 
-    // ---- U. prune, advance, recombine (every wave, lane j = slot j) ----
+    // ---- U. prune, recombine, take the new beam (every wave, lane j = slot j) ----
     {
       const int nsel = min(K, nfin);
       const bool valid = j < nsel;
-      float x = kNegInf;
-      uint32_t idx = 0u, lmt = 0u, btk = 0u;
-      if (valid) {
-        const uint4 e = s_res[mpar][j];
-        x = __uint_as_float(e.x);
-        idx = e.y;
-        lmt = e.z;
-        btk = e.w;
-      }
-      const uint32_t par = valid ? idx / static_cast<uint32_t>(W) : 0u;
-      const int c = valid ? static_cast<int>(idx - par * static_cast<uint32_t>(W)) : V;
-      const int ipar = static_cast<int>(par);
-      // parent fields (every lane takes part in the exchange)
-      const int lastp = __shfl(last, ipar);
-      const uint64_t hashp = __shfl(hash, ipar);
-      const int lenp = __shfl(len, ipar);
-      const uint32_t lmsp = __shfl(lms, ipar), btsp = __shfl(bts, ipar);
-      uint32_t pb[NLA], pc[NLA];
-      float pbo[NLA];
+      uint32_t rec[RW];
 #pragma unroll
-      for (int l = 0; l < NL; ++l) {
-        pb[l] = __shfl(lvb[l], ipar);
-        pc[l] = __shfl(lvc[l], ipar);
-        pbo[l] = __shfl(lvbo[l], ipar);
-      }
-      uint32_t pbb = 0u, pbc = 0u;
-      int32_t pbp = 0;
-      if (HAS_BT) {
-        pbb = __shfl(btb, ipar);
-        pbc = __shfl(btc, ipar);
-        pbp = __shfl(btpot, ipar);
-      }
-      const bool emit = valid && c != V && c != lastp;
-      // chain headers of emitting winners (issued early, used at the end)
-      LmLevel hh[NLA];
-#pragma unroll
-      for (int l = 0; l < NL; ++l) hh[l] = p.lm_states[static_cast<size_t>(emit ? lmt : p.lm_bos_state) * NL + l];
-      BtNode nd{0u, 0u, 0u, 0u};
-      if (HAS_BT) nd = p.bt_nodes[emit ? (btk & kBtChildMask) : 0u];
+      for (int w = 0; w < RW; ++w) rec[w] = 0u;
+      if (valid) load_rec(s_rec + (rcur ^ 1) * (kMaxK * RW) + j * RW, rec);
+      float x = valid ? __uint_as_float(rec[kRX]) : kNegInf;
       // prune (Algorithm 1: below best - theta -> -inf)
       const float best = rdlane(x, 0);
       const float lim = best - p.theta;
       if (valid && x < lim) x = kNegInf;
+      const bool emit = valid && rec[kREmit] != 0u;
       const bool emit_fin = x != kNegInf && emit;
-      const int32_t nlast = valid ? c : V;
-      const int32_t nlen = valid ? lenp + (emit ? 1 : 0) : 0;
-      const uint64_t nhash = valid ? (emit ? mix_token(hashp, static_cast<uint32_t>(c)) : hashp) : 0ull;
-      const uint32_t nlms = valid ? ((HAS_LM && emit) ? lmt : lmsp) : 0u;
-      const uint32_t nbts = valid ? ((HAS_BT && emit) ? (btk & kBtChildMask) : btsp) : 0u;
+      const int32_t nlast = valid ? static_cast<int32_t>(rec[kRLast]) : V;
+      const int32_t nlen = static_cast<int32_t>(rec[kRLen]);
       // recombination: same transcript hash, length and ends-in-blank flag as
       // a live lower slot
       const bool alive0 = valid && x != kNegInf;
       const uint32_t meta = (static_cast<uint32_t>(nlen) & 0x3FFFFFFFu) | ((nlast == V ? 1u : 0u) << 30);
-      const uint64_t amask0 = __ballot(alive0);
       bool dup = false;
-      {
-        uint64_t mr = amask0 & ~(1ull << 63);  // the top lane can never be the lower slot of a pair
+      if (K <= 16) {
+        // the K slots sit in the first 16-lane row: compare with lanes j-1 ..
+        // j-(K-1) through row shifts; a dead lane's key has bit 31 set and
+        // lanes shifted in from outside the row read all ones, so neither
+        // matches a live slot
+        const uint32_t mkey = meta | (alive0 ? 0u : 0x80000000u);
+        recomb_shifts<1>(K, rec[kRHlo], rec[kRHhi], mkey, dup);
+        dup = dup && alive0;
+      } else {
+        uint64_t mr = __ballot(alive0) & ~(1ull << 63);  // the top lane is never the lower slot
         while (mr) {
           const int i = static_cast<int>(__builtin_ctzll(mr));
           mr &= mr - 1ull;
-          const uint32_t hlo = rdlane(static_cast<uint32_t>(nhash), i);
-          const uint32_t hhi = rdlane(static_cast<uint32_t>(nhash >> 32), i);
+          const uint32_t hlo = rdlane(rec[kRHlo], i);
+          const uint32_t hhi = rdlane(rec[kRHhi], i);
           const uint32_t mi = rdlane(meta, i);
-          dup = dup || (j > i && alive0 && static_cast<uint32_t>(nhash) == hlo &&
-                        static_cast<uint32_t>(nhash >> 32) == hhi && meta == mi);
+          dup = dup || (j > i && alive0 && rec[kRHlo] == hlo && rec[kRHhi] == hhi && meta == mi);
         }
       }
       if (dup) x = kNegInf;
       const bool nalive = alive0 && !dup;
-      if (wave == 0 && j < K)
-        bpb[static_cast<size_t>(t) * K + j] = valid ? static_cast<int32_t>((par << 16) | static_cast<uint32_t>(c)) : -1;
+      if (wave == 0 && j < K) bpb[static_cast<size_t>(t) * K + j] = valid ? static_cast<int32_t>(rec[kRBp]) : -1;
       // new state
       sc = x;
       last = nlast;
       len = nlen;
-      hash = nhash;
-      lms = nlms;
-      bts = nbts;
       alive = nalive;
       int32_t acnt = 0;
 #pragma unroll
       for (int l = 0; l < NL; ++l) {
-        lvb[l] = nalive ? (emit ? hh[l].begin : pb[l]) : 0u;
-        lvc[l] = nalive ? (emit ? hh[l].count : pc[l]) : 0u;
-        lvbo[l] = nalive ? (emit ? hh[l].bo : pbo[l]) : 0.0f;
+        lvb[l] = nalive ? rec[kRLvb + l] : 0u;
+        lvc[l] = nalive ? rec[kRLvc + l] : 0u;
+        lvbo[l] = nalive ? __uint_as_float(rec[kRLvbo + l]) : 0.0f;
         acnt += static_cast<int32_t>(lvc[l] & ~kExists);
       }
       if (HAS_BT) {
-        btb = nalive ? (emit ? nd.list_begin : pbb) : 0u;
-        btc = nalive ? (emit ? nd.list_count : pbc) : 0u;
-        btpot = nalive ? (emit ? static_cast<int32_t>(nd.pot & 0xFFu) : pbp) : 0;
+        btb = nalive ? rec[kRBtb] : 0u;
+        btc = nalive ? rec[kRBtc] : 0u;
+        btpot = nalive ? static_cast<int32_t>(rec[kRBtp]) : 0;
       }
       if (want_stats && wave == 0) {
         // chain work of the next frame (alive beams) and this frame's
@@ -951,8 +1029,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
           }
           if (HAS_BT) {
-            // boosting statistics need the node record of inherited states too
-            const BtNode pn = emit ? nd : p.bt_nodes[bts];
+            const BtNode pn = p.bt_nodes[rec[kRBts]];
             s_bn = pn.pot >> 8;
             s_ba = pn.chain_arcs;
           }
@@ -964,6 +1041,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         if (s_ba) atomicAdd(&s_st[4], static_cast<unsigned long long>(s_ba));
         if (emit_fin) atomicAdd(&s_st[5], 1ull);
       }
+      rcur ^= 1;
       // live positions and beam records for the next frame
       const uint64_t amask = __ballot(nalive);
       const int na = __popcll(amask);
