@@ -18,34 +18,37 @@
 // cross-lane chains, barriers), so MFMA is not used.
 //
 // Every wave keeps the whole beam (slot j in lane j: score, last label,
-// transcript hash, LM/boosting states and their backoff chains) in registers.
-// Each wave runs the beam update itself on the same inputs, so the next
-// frame's fill starts without a hand-off between waves.  Per frame (one
-// chunk when K*V fits the LDS key rows, e.g. K=8, V=1024), with 4 barriers:
+// length, LM/boosting chain headers) in registers and runs the beam update
+// itself, so the next frame's fill starts without a hand-off between waves.
+// Per-slot state records (transcript hash, LM/boosting states, chains) live
+// in LDS, double-buffered by frame.  Per frame (one chunk when K*V fits the
+// LDS key rows, e.g. K=8, V=1024), with 4 barriers:
 //   F. fill: the explicit continuations of every live beam's LM backoff chain
 //      (and its merged boosting continuation list) are cut into tiles of 64
-//      and spread over all waves; each lane loads one arc per tile and
-//      scatters it into an LDS [beam][token] row: LM entries are 64-bit
-//      (generation | order | staging slot : alpha*value) combined with an
-//      atomic max, so the highest-order n-gram wins in any order; boosting
-//      entries are generation-tagged keys.  Entries of older generations read
-//      as absent, so the rows are never cleared (except when the 6-bit
-//      generation wraps).
+//      that never straddle a (beam, level) run and are dealt to all waves;
+//      each lane loads one arc per tile and scatters it into an LDS
+//      [beam][token] row: LM entries are 64-bit (generation | order | staging
+//      slot : alpha*value) combined with an atomic max, so the highest-order
+//      n-gram wins in any order; boosting entries are generation-tagged keys.
+//      Entries of older generations read as absent, so the rows are never
+//      cleared (except when the 6-bit generation wraps).
 //   C. candidates: each lane scores its labels for every beam of the chunk in
-//      registers (beam data by readlane), resolving the LM value from the row
-//      or from the unigram + backoff fold, and publishes the maximum of each
-//      16-lane row.
-//   T. filter: the K-th largest of those disjoint-group maxima is a lower
-//      bound on the K-th best candidate; candidates at or above it (a few
-//      dozen) are appended to a survivor pool in LDS.
+//      registers (beam data by broadcast LDS reads), resolving the LM value
+//      from the row or from the unigram + backoff fold, and publishes the
+//      maxima of disjoint lane groups.
+//   T. filter: the K-th largest group maximum, and with K live slots the
+//      smallest blank score, bound the K-th best candidate from below;
+//      candidates at or above the bound (a few dozen) go to a survivor pool
+//      in LDS.
 //   R. rank: the pool (survivors plus K reserved entries holding the blank
 //      candidates, or the best K of earlier chunks) is ranked exactly by
 //      (score desc, flat index asc): each wave ranks an eighth of the pool
-//      against all of it with ballots, and the best K go to a reserved region
-//      in rank order.
-//   U. update: prune, advance (hash of the collapsed transcript, LM/boosting
-//      states, chain headers fetched for emitting winners), recombine, plan
-//      the next frame's chunks, write back-pointers to HBM.
+//      against all of it with ballots.  The owner of each winner builds its
+//      successor record from the parent's record (hash of the collapsed
+//      transcript, LM/boosting states, chain headers of an emitted token,
+//      fetched while the ranking runs).
+//   U. update: prune, recombine, take the new beam into registers, plan the
+//      next frame's chunks, write back-pointers to HBM.
 // Large beams (K*V above the key rows) repeat F/C/T/R per chunk of beams with
 // a running bound.  A survivor pool overflow falls back to an exact
 // extraction.  After the last frame the best beam is traced back through the
@@ -187,6 +190,7 @@ __device__ __forceinline__ int wave_incl_scan(int v, int lane) {
 
 // maximum over each 16-lane row, valid in the row's last lane
 __device__ __forceinline__ float fmax_sel(float a, float b) { return (b > a) ? b : a; }
+__device__ __forceinline__ float fmin_sel(float a, float b) { return (b < a) ? b : a; }
 __device__ __forceinline__ float row_max_last(float v) {
   const float ni = -__builtin_huge_valf();
   v = fmax_sel(v, dpp_movf<kDppRowShr1>(v, ni));
@@ -234,18 +238,16 @@ __device__ __forceinline__ float bitonic_levels(float v, int lane) {
   if constexpr (k < N) v = bitonic_levels<N, k * 2>(v, lane);
   return v;
 }
-// Recombination probe at distance D = 1..15 (lane j against lane j-D of its
-// 16-lane row), for the D below the beam size.
-template <int D>
-__device__ __forceinline__ void recomb_shifts(int K, uint32_t hlo, uint32_t hhi, uint32_t mkey, bool& dup) {
-  if (D < K) {  // wave-uniform
-    constexpr int kCtrl = 0x110 + D;  // row_shr:D
-    const uint32_t ol = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(hlo), kCtrl, 0xF, 0xF, false));
-    const uint32_t oh = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(hhi), kCtrl, 0xF, 0xF, false));
-    const uint32_t om = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(mkey), kCtrl, 0xF, 0xF, false));
-    dup = dup || (ol == hlo && oh == hhi && om == mkey);
-    if constexpr (D < 15) recomb_shifts<D + 1>(K, hlo, hhi, mkey, dup);
-  }
+// Recombination probes at distances D = 1..DMAX: lane j against lane j-D of
+// its 16-lane row.  Lanes shifted in from outside the row read all ones.
+template <int D, int DMAX>
+__device__ __forceinline__ bool recomb_shifts(uint32_t klo, uint32_t khi) {
+  constexpr int kCtrl = 0x110 + D;  // row_shr:D
+  const uint32_t ol = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(klo), kCtrl, 0xF, 0xF, false));
+  const uint32_t oh = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(khi), kCtrl, 0xF, 0xF, false));
+  bool m = ((static_cast<uint64_t>(oh) << 32) | ol) == ((static_cast<uint64_t>(khi) << 32) | klo);
+  if constexpr (D < DMAX) m = m || recomb_shifts<D + 1, DMAX>(klo, khi);
+  return m;
 }
 
 // Bitonic sort of one value per lane within groups of N lanes, descending.
@@ -297,7 +299,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keep it in an SGPR
   const int b = blockIdx.x;
   const int V = p.V, W = V + 1, K = p.K, T = p.T;
   const int kcmax = min(K, KSEG);
@@ -329,7 +331,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     rD[j] = kNegInf;
   }
   const bool blank_lane = (wave == 0) && (lane < K);
-  float rBlankN = (L > 0 && blank_lane) ? Db[V] : 0.0f;
+  float rBlankN = (L > 0 && lane < K) ? Db[V] : 0.0f;
   float rBlank = 0.0f;
 
   // ---- beam state: slot j in lane j, replicated in every wave ----
@@ -382,6 +384,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   int rcur = 0;  // s_rec buffer holding the current beam
   // record helpers
   auto load_rec = [&](const uint32_t* src, uint32_t (&r)[RW]) {
+    src = static_cast<const uint32_t*>(__builtin_assume_aligned(src, 16));
 #pragma unroll
     for (int w4 = 0; w4 < RW; w4 += 4) {
       const uint4 v = *reinterpret_cast<const uint4*>(src + w4);
@@ -392,17 +395,20 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     }
   };
   auto store_rec = [&](uint32_t* dst, const uint32_t (&r)[RW]) {
+    dst = static_cast<uint32_t*>(__builtin_assume_aligned(dst, 16));
 #pragma unroll
     for (int w4 = 0; w4 < RW; w4 += 4) *reinterpret_cast<uint4*>(dst + w4) = make_uint4(r[w4], r[w4 + 1], r[w4 + 2], r[w4 + 3]);
   };
-  // successor of a selected candidate (flat index idx, resolved LM target,
-  // boosting key) from its parent's record: first the parent, the emitted
-  // flag and the chain headers of an emitted token (global loads in flight),
-  // then the record
+  // Successor of a selected candidate (flat index idx, resolved LM target,
+  // boosting key) from its parent's record.  succ_begin reads the parent and
+  // starts the chain-header loads of an emitted token; succ_end builds the
+  // record in every lane (branch-free, so the loads stay where they were
+  // issued) and the caller stores it for the winners.
   struct Succ {
     uint32_t par, lmt, btk;
     int c;
     bool emit;
+    uint32_t r[RW];
     LmLevel hh[NLA];
     BtNode nd;
   };
@@ -411,43 +417,40 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     sp.c = act ? static_cast<int>(idx - sp.par * static_cast<uint32_t>(W)) : V;
     sp.lmt = lmt;
     sp.btk = btk;
-    const int lastp = static_cast<int>(prec[sp.par * RW + kRLast]);
-    sp.emit = act && sp.c != V && sp.c != lastp;
+    load_rec(prec + sp.par * RW, sp.r);
+    sp.emit = act && sp.c != V && sp.c != static_cast<int>(sp.r[kRLast]);
 #pragma unroll
     for (int l = 0; l < NL; ++l)
       sp.hh[l] = p.lm_states[static_cast<size_t>(sp.emit ? lmt : p.lm_bos_state) * NL + l];
     sp.nd = BtNode{0u, 0u, 0u, 0u};
     if (HAS_BT) sp.nd = p.bt_nodes[sp.emit ? (btk & kBtChildMask) : 0u];
   };
-  auto succ_end = [&](const Succ& sp, uint32_t xbits, const uint32_t* prec, uint32_t* dst) {
-    uint32_t r[RW];
-    load_rec(prec + sp.par * RW, r);
+  auto succ_end = [&](Succ& sp, uint32_t xbits) {
+    uint32_t* r = sp.r;
     const bool e = sp.emit;
     uint64_t h = (static_cast<uint64_t>(r[kRHhi]) << 32) | r[kRHlo];
-    if (e) h = mix_token(h, static_cast<uint32_t>(sp.c));
+    const uint64_t hm = mix_token(h, static_cast<uint32_t>(sp.c));
+    h = e ? hm : h;
     r[kRX] = xbits;
     r[kRBp] = (sp.par << 16) | static_cast<uint32_t>(sp.c);
     r[kRHlo] = static_cast<uint32_t>(h);
     r[kRHhi] = static_cast<uint32_t>(h >> 32);
     r[kRLen] += e ? 1u : 0u;
     r[kRLast] = static_cast<uint32_t>(sp.c);
-    if (HAS_LM && e) r[kRLms] = sp.lmt;
-    if (HAS_BT && e) r[kRBts] = sp.btk & kBtChildMask;
+    if (HAS_LM) r[kRLms] = e ? sp.lmt : r[kRLms];
+    if (HAS_BT) r[kRBts] = e ? (sp.btk & kBtChildMask) : r[kRBts];
     r[kREmit] = e ? 1u : 0u;
-    if (HAS_BT && e) {
-      r[kRBtb] = sp.nd.list_begin;
-      r[kRBtc] = sp.nd.list_count;
-      r[kRBtp] = sp.nd.pot & 0xFFu;
+    if (HAS_BT) {
+      r[kRBtb] = e ? sp.nd.list_begin : r[kRBtb];
+      r[kRBtc] = e ? sp.nd.list_count : r[kRBtc];
+      r[kRBtp] = e ? (sp.nd.pot & 0xFFu) : r[kRBtp];
     }
 #pragma unroll
     for (int l = 0; l < NL; ++l) {
-      if (e) {
-        r[kRLvb + l] = sp.hh[l].begin;
-        r[kRLvc + l] = sp.hh[l].count;
-        r[kRLvbo + l] = __float_as_uint(sp.hh[l].bo);
-      }
+      r[kRLvb + l] = e ? sp.hh[l].begin : r[kRLvb + l];
+      r[kRLvc + l] = e ? sp.hh[l].count : r[kRLvc + l];
+      r[kRLvbo + l] = e ? __float_as_uint(sp.hh[l].bo) : r[kRLvbo + l];
     }
-    store_rec(dst, r);
   };
 
   for (int i = tid; i < kOffTgt; i += kThreads) s_big[i] = 0u;
@@ -507,7 +510,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         const int c = tid + jj * kThreads;
         if (c < V) rDn[jj] = __builtin_nontemporal_load(rowp + c);
       }
-      if (blank_lane) rBlankN = __builtin_nontemporal_load(rowp + V);
+      if (lane < K) rBlankN = __builtin_nontemporal_load(rowp + V);
     }
     float tau_run = kNegInf;
     int nfin = 0;
@@ -735,9 +738,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       }
       // Maxima of disjoint lane groups are distinct candidates, so the K-th
       // largest of at least K group maxima bounds the K-th best candidate
-      // from below.  K <= 32: the 32 rows of 16 lanes; otherwise 64 groups of
-      // 8 lanes.
-      if (K <= 32) {
+      // from below.  K <= 8: the 8 wave maxima; K <= 32: the 32 rows of 16
+      // lanes; otherwise 64 groups of 8 lanes.
+      if (K <= 8) {
+        const float g = row_max_last(lmax);
+        const float g2 = fmax_sel(fmax_sel(rdlane(g, 15), rdlane(g, 31)), fmax_sel(rdlane(g, 47), rdlane(g, 63)));
+        if (lane == 0) s_top[wave] = g2;
+      } else if (K <= 32) {
         const float g = row_max_last(lmax);
         if ((lane & 15) == 15) s_top[wave * 4 + (lane >> 4)] = g;
       } else {
@@ -749,14 +756,27 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       // ---- T. bound and filter ----
       {
         float tc;
-        if (K <= 32) {
+        if (K <= 8) {
+          const float v = wave_sort_desc<8>(lane < 8 ? s_top[lane] : kNegInf, lane);
+          tc = rdlane(v, K - 1);
+        } else if (K <= 32) {
           const float v = wave_sort_desc<32>(lane < 32 ? s_top[lane] : kNegInf, lane);
           tc = rdlane(v, K - 1);
         } else {
           const float v = wave_sort_desc<64>(s_top[lane], lane);
           tc = rdlane(v, K - 1);
         }
-        const float tau = fmaxf(tau_run, tc);
+        // the blank candidates are exact: with K live slots the smallest
+        // blank score also bounds the K-th best from below
+        float tb = (lane < K) ? sc + rBlank : __builtin_huge_valf();
+        tb = fmin_sel(tb, xor_lane(tb, 1, lane));
+        tb = fmin_sel(tb, xor_lane(tb, 2, lane));
+        tb = fmin_sel(tb, xor_lane(tb, 4, lane));
+        if (K > 8) tb = fmin_sel(tb, xor_lane(tb, 8, lane));
+        if (K > 16) tb = fmin_sel(tb, xor_lane(tb, 16, lane));
+        if (K > 32) tb = fmin_sel(tb, xor_lane(tb, 32, lane));
+        const float tblank = rdlane(tb, 0);
+        const float tau = fmaxf(fmaxf(tau_run, tc), tblank);
         uint32_t qmask = 0u;
 #pragma unroll
         for (int r = 0; r < NC; ++r) qmask |= (cand[r] >= tau && cand[r] != kNegInf) ? (1u << r) : 0u;
@@ -821,11 +841,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               const int rk = __popcll(__ballot(xq > xs || (xq == xs && eq.y < is)));
               myrank = ((lane >> 3) == u) ? rk : myrank;
             }
-            if (own && myrank < K) {
-              if (last_chunk)
-                succ_end(sp, eq.x, prec, nrec + myrank * RW);
-              else
-                s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
+            if (last_chunk) {
+              succ_end(sp, eq.x);
+              if (own && myrank < K) store_rec(nrec + myrank * RW, sp.r);
+            } else if (own && myrank < K) {
+              s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
             }
           } else {
             // blocks of 64 entries: this wave ranks entries qb + (wave + 8u)
@@ -869,7 +889,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               if (last_chunk) {
                 Succ sp;
                 succ_begin(win, eq.y, lmt, eq.w, prec, sp);
-                if (win) succ_end(sp, eq.x, prec, nrec + myrank * RW);
+                succ_end(sp, eq.x);
+                if (win) store_rec(nrec + myrank * RW, sp.r);
               } else if (win) {
                 s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
               }
@@ -940,7 +961,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             if (act) e = s_res[Q][lane];
             Succ sp;
             succ_begin(act, e.y, e.z, e.w, prec, sp);
-            if (act) succ_end(sp, e.x, prec, nrec + lane * RW);
+            succ_end(sp, e.x);
+            if (act) store_rec(nrec + lane * RW, sp.r);
           }
         }
         // ranks [nfin, K) hold no candidate (the next chunk reads all K)
@@ -976,13 +998,16 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       const uint32_t meta = (static_cast<uint32_t>(nlen) & 0x3FFFFFFFu) | ((nlast == V ? 1u : 0u) << 30);
       bool dup = false;
       if (K <= 16) {
-        // the K slots sit in the first 16-lane row: compare with lanes j-1 ..
-        // j-(K-1) through row shifts; a dead lane's key has bit 31 set and
-        // lanes shifted in from outside the row read all ones, so neither
-        // matches a live slot
-        const uint32_t mkey = meta | (alive0 ? 0u : 0x80000000u);
-        recomb_shifts<1>(K, rec[kRHlo], rec[kRHhi], mkey, dup);
-        dup = dup && alive0;
+        // The K slots sit in the first 16-lane row: compare each with the
+        // slots below it through row shifts.  The key folds the length and
+        // the ends-in-blank flag into the 64-bit transcript hash (a false
+        // merge needs a 64-bit collision, as for the hash itself); dead
+        // slots use all ones and are never merged into.
+        uint64_t key = ((static_cast<uint64_t>(rec[kRHhi]) << 32) | rec[kRHlo]) ^
+                       (static_cast<uint64_t>(meta + 1u) * 0xD6E8FEB86659FD93ull);
+        if (!alive0) key = ~0ull;
+        const uint32_t klo = static_cast<uint32_t>(key), khi = static_cast<uint32_t>(key >> 32);
+        dup = (K <= 8 ? recomb_shifts<1, 7>(klo, khi) : recomb_shifts<1, 15>(klo, khi)) && alive0;
       } else {
         uint64_t mr = __ballot(alive0) & ~(1ull << 63);  // the top lane is never the lower slot
         while (mr) {
