@@ -168,6 +168,27 @@ int ctcbeam_decode_ex(const float* logprobs, const int32_t* lengths, int B, int 
                       int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
                       hipStream_t stream, const ctcbeam_opts* opts);
 
+/*
+ * N-best output (Algorithm 1 keeps K hypotheses per utterance in the batch;
+ * Sec. III-A: any of them can be read back from the hypothesis trie): the
+ * same search as ctcbeam_decode_ex, returning every beam slot's final
+ * hypothesis after LM.Final instead of the best one only.
+ *   nbest_tokens  : device int32 [B, K, T]; row r of utterance b holds the
+ *                   collapsed transcript of the r-th best slot, -1 padded
+ *   nbest_lengths : device int32 [B, K]; 0 for a dead slot
+ *   nbest_scores  : device fp32 [B, K]; descending, ties in slot order;
+ *                   -inf for a dead slot (dead slots sort last)
+ * Row 0 equals ctcbeam_decode_ex's output.  Rows are not deduplicated beyond
+ * the recombination of Algorithm 1 (two slots can hold the same transcript,
+ * one ending in blank and one not).  Workspace, stream, opts, ownership and
+ * errors as for ctcbeam_decode_ex; all three outputs are required.
+ */
+int ctcbeam_decode_nbest(const float* logprobs, const int32_t* lengths, int B, int T, int V,
+                         int K, float alpha, float beta, float boost_w, const ctcbeam_lm* lm,
+                         const ctcbeam_boost* boost, void* workspace, size_t workspace_bytes,
+                         int32_t* nbest_tokens, int32_t* nbest_lengths, float* nbest_scores,
+                         hipStream_t stream, const ctcbeam_opts* opts);
+
 /* Status bits of the last decode that used `workspace` (synchronises
  * `stream`): bit 0 = a length was clamped, bit 1 = internal traceback
  * mismatch, bit 2 = internal staging overflow. */

@@ -66,7 +66,7 @@ def _load():
     lib.oracle_decode.restype = ctypes.c_int
     lib.oracle_decode.argtypes = [P, P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                   ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
-                                  P, P, ctypes.c_int, P, P, P, P, P, P, P]
+                                  P, P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P]
     _lib = lib
     return lib
 
@@ -164,8 +164,12 @@ class BT:
 def decode(logprobs: np.ndarray, lengths, K: int, alpha: float = 0.0, beta: float = 0.0,
            boost_w: float = 0.0, theta: float = math.inf, lm: Optional[LM] = None,
            bt: Optional[BT] = None, n_threads: int = 1, want_align: bool = False,
-           want_trace: bool = False, want_counters: bool = False) -> dict:
-    """Run the oracle on host arrays.  logprobs: fp32 [B, T, V+1] (blank = V)."""
+           want_trace: bool = False, want_counters: bool = False, want_nbest: bool = False) -> dict:
+    """Run the oracle on host arrays.  logprobs: fp32 [B, T, V+1] (blank = V).
+
+    want_nbest adds every slot's final hypothesis ordered by final score
+    (lowest slot on ties; dead slots last, empty, -inf): nbest_tokens
+    [B, K, T] (-1 padded), nbest_lengths [B, K], nbest_scores [B, K]."""
     lib = _load()
     lp = np.ascontiguousarray(logprobs, dtype=np.float32)
     B, T, W = lp.shape
@@ -179,10 +183,14 @@ def decode(logprobs: np.ndarray, lengths, K: int, alpha: float = 0.0, beta: floa
     bp = np.full((B, T, K), -1, dtype=np.int32) if want_trace else None
     ss = np.full((B, T, K), np.nan, dtype=np.float32) if want_trace else None
     cnt = np.zeros((B, 8), dtype=np.int64) if want_counters else None
+    nbt = np.empty((B, K, T), dtype=np.int32) if want_nbest else None
+    nbl = np.empty((B, K), dtype=np.int32) if want_nbest else None
+    nbs = np.empty((B, K), dtype=np.float32) if want_nbest else None
     rc = lib.oracle_decode(_ptr(lp), _ptr(ln), B, T, V, int(K), float(alpha), float(beta),
                            float(boost_w), float(theta), lm._h if lm else None,
                            bt._h if bt else None, int(n_threads), _ptr(toks), _ptr(lens),
-                           _ptr(scores), _ptr(align), _ptr(bp), _ptr(ss), _ptr(cnt))
+                           _ptr(scores), _ptr(align), _ptr(bp), _ptr(ss), _ptr(cnt),
+                           _ptr(nbt), _ptr(nbl), _ptr(nbs))
     if rc != 0:
         raise ValueError(f"oracle_decode returned {rc}")
     out = dict(tokens=toks, lengths=lens, scores=scores)
@@ -193,4 +201,8 @@ def decode(logprobs: np.ndarray, lengths, K: int, alpha: float = 0.0, beta: floa
         out["slot_scores"] = ss
     if want_counters:
         out["counters"] = cnt
+    if want_nbest:
+        out["nbest_tokens"] = nbt
+        out["nbest_lengths"] = nbl
+        out["nbest_scores"] = nbs
     return out

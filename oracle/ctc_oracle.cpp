@@ -28,7 +28,11 @@
 //     with its own score (max, Viterbi) and dead slots stay in place;
 //   * final: alive scores get fl(alpha * LM(k, </s>)) (Alg. 1, LM.Final);
 //   * output: best slot, lowest index on ties; if its score is -inf the
-//     transcript is empty and the score -inf.
+//     transcript is empty and the score -inf;
+//   * N-best output (all K final hypotheses, the batched-hypotheses result of
+//     Alg. 1): the slots ordered by final score descending, lowest slot on
+//     ties, each with its transcript; dead slots come last with an empty
+//     transcript and score -inf.
 //
 // LM(k,c): ARPA backoff in natural log (Sec. II "NGPU-LM"; Sec. IV-A builds the
 // LM from an ARPA file).  P(c|h) = p(h c) if that n-gram exists, otherwise
@@ -207,6 +211,9 @@ struct DecodeArgs {
   int32_t* bp_index;      // [B,T,K] flat candidate index of each slot (nullable)
   float* slot_scores;     // [B,T,K] slot scores after recombination (nullable)
   int64_t* counters;      // [B,8] (nullable)
+  int32_t* nbest_tokens;  // [B,K,T] -1 padded (nullable: no N-best output)
+  int32_t* nbest_lengths; // [B,K]
+  float* nbest_scores;    // [B,K]
 };
 
 void decode_one(const DecodeArgs& a, int b) {
@@ -344,6 +351,21 @@ void decode_one(const DecodeArgs& a, int b) {
   }
   a.out_scores[b] = score;
   if (a.out_lengths) a.out_lengths[b] = n_out;
+  if (a.nbest_tokens) {
+    std::vector<int> order(K);
+    for (int k = 0; k < K; ++k) order[k] = k;
+    std::stable_sort(order.begin(), order.end(), [&](int p, int q) { return hyp[p].s > hyp[q].s; });
+    for (int r = 0; r < K; ++r) {
+      const Hyp& h = hyp[order[r]];
+      const bool live = h.s != NEG_INF;
+      int32_t* nt = a.nbest_tokens + (static_cast<size_t>(b) * K + r) * T;
+      for (int t = 0; t < T; ++t) nt[t] = -1;
+      const int n = live ? static_cast<int>(h.y.size()) : 0;
+      for (int i = 0; i < n; ++i) nt[i] = h.y[i];
+      a.nbest_lengths[static_cast<size_t>(b) * K + r] = n;
+      a.nbest_scores[static_cast<size_t>(b) * K + r] = h.s;
+    }
+  }
   if (a.counters)
     for (int i = 0; i < 8; ++i) a.counters[static_cast<size_t>(b) * 8 + i] = cnt[i];
 }
@@ -451,19 +473,25 @@ int oracle_bt_pot(const void* bt, const int32_t* q, int nq) {
 
 // Batched beam search over host arrays (same argument meaning as the device
 // decoder; theta = +inf disables pruning).  n_threads > 1 spreads utterances
-// over std::threads.  Returns 0 on success, 1 on invalid arguments.
+// over std::threads.  Optional outputs (null to skip): the best path's frame
+// labels, per-frame back-pointer indices and slot scores, work counters, and
+// the N-best list (tokens [B,K,T], lengths [B,K], scores [B,K]).  Returns 0 on
+// success, 1 on invalid arguments.
 int oracle_decode(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K,
                   float alpha, float beta, float boost_w, float theta, const void* lm, const void* bt,
                   int n_threads, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
-                  int32_t* out_align, int32_t* bp_index, float* slot_scores, int64_t* counters) {
+                  int32_t* out_align, int32_t* bp_index, float* slot_scores, int64_t* counters,
+                  int32_t* nbest_tokens, int32_t* nbest_lengths, float* nbest_scores) {
   if (B < 0 || T < 0 || V < 1 || K < 1 || !out_tokens || !out_scores) return 1;
+  if (nbest_tokens && (!nbest_lengths || !nbest_scores)) return 1;
   if (B > 0 && (!logprobs || !lengths)) return 1;
   const OracleLM* plm = static_cast<const OracleLM*>(lm);
   if (plm && plm->V != V) return 1;
   const OracleBT* pbt = static_cast<const OracleBT*>(bt);
   if (pbt && pbt->V != V) return 1;
   DecodeArgs a{logprobs, lengths, B, T, V, K, alpha, beta, boost_w, theta, plm, pbt,
-               out_tokens, out_lengths, out_scores, out_align, bp_index, slot_scores, counters};
+               out_tokens, out_lengths, out_scores, out_align, bp_index, slot_scores, counters,
+               nbest_tokens, nbest_lengths, nbest_scores};
   if (n_threads <= 1 || B <= 1) {
     for (int b = 0; b < B; ++b) decode_one(a, b);
     return 0;

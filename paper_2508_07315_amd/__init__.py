@@ -76,6 +76,8 @@ def _load():
     lib.ctcbeam_decode.argtypes = dec
     lib.ctcbeam_decode_ex.restype = I
     lib.ctcbeam_decode_ex.argtypes = dec + [P]
+    lib.ctcbeam_decode_nbest.restype = I
+    lib.ctcbeam_decode_nbest.argtypes = dec + [P]
     lib.ctcbeam_query_status.restype = I
     lib.ctcbeam_query_status.argtypes = [P, I, P, ctypes.POINTER(ctypes.c_uint32)]
     lib.ctcbeam_lm_tables.restype = I
@@ -321,6 +323,53 @@ def ctcbeam_decode(logprobs, lengths, K: int, alpha: float = 0.0, beta: float = 
                              out_tokens, out_lengths, out_scores, stream)
 
 
+def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: float = 0.0,
+                         boost_w: float = 0.0, lm: Optional[LM] = None,
+                         boost: Optional[Boost] = None, workspace=None, nbest_tokens=None,
+                         nbest_lengths=None, nbest_scores=None, stream=None,
+                         theta: float = math.inf, stats=None):
+    """Enqueue one N-best decode on ``stream`` (default: torch's current stream).
+
+    Same inputs as ``ctcbeam_decode_ex``.  Returns (tokens [B,K,T] int32 with
+    -1 padding, lengths [B,K] int32, scores [B,K] float32 descending,
+    workspace uint8); row 0 of each utterance is the 1-best result."""
+    import torch
+    lib = _load()
+    if logprobs.dim() != 3:
+        raise ValueError("logprobs must be [B, T, V+1]")
+    B, T, W = (int(x) for x in logprobs.shape)
+    V = W - 1
+    K = int(K)
+    dev = logprobs.device
+    if nbest_tokens is None:
+        nbest_tokens = torch.empty((B, K, T), dtype=torch.int32, device=dev)
+    if nbest_lengths is None:
+        nbest_lengths = torch.empty((B, K), dtype=torch.int32, device=dev)
+    if nbest_scores is None:
+        nbest_scores = torch.empty((B, K), dtype=torch.float32, device=dev)
+    need = ctcbeam_workspace_bytes(B, T, K)
+    if workspace is None:
+        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
+    ws = _dptr(workspace, torch.uint8, "workspace")
+    opts = None
+    if (theta is not None and not math.isinf(theta)) or stats is not None:
+        o = _Opts()
+        o.prune_theta = float(theta if theta is not None else math.inf)
+        o.stats = None if stats is None else _dptr(stats, torch.int64, "stats", (B, 8)).value
+        opts = ctypes.byref(o)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev).cuda_stream
+    rc = lib.ctcbeam_decode_nbest(
+        _dptr(logprobs, torch.float32, "logprobs"), _dptr(lengths, torch.int32, "lengths", (B,)),
+        B, T, V, K, float(alpha), float(beta), float(boost_w),
+        lm.handle if lm is not None else None, boost.handle if boost is not None else None,
+        ws, int(workspace.numel()), _dptr(nbest_tokens, torch.int32, "nbest_tokens", (B, K, T)),
+        _dptr(nbest_lengths, torch.int32, "nbest_lengths", (B, K)),
+        _dptr(nbest_scores, torch.float32, "nbest_scores", (B, K)), ctypes.c_void_p(stream), opts)
+    _check(rc)
+    return nbest_tokens, nbest_lengths, nbest_scores, workspace
+
+
 def ctcbeam_query_status(workspace, B: int, stream=None) -> int:
     import torch
     if stream is None:
@@ -334,4 +383,10 @@ def ctcbeam_query_status(workspace, B: int, stream=None) -> int:
 def decode(logprobs, lengths, K: int, **kw):
     """Convenience: returns (tokens, lengths, scores) device tensors."""
     tok, ln, sc, _ = ctcbeam_decode_ex(logprobs, lengths, K, **kw)
+    return tok, ln, sc
+
+
+def decode_nbest(logprobs, lengths, K: int, **kw):
+    """Convenience: returns N-best (tokens [B,K,T], lengths [B,K], scores [B,K])."""
+    tok, ln, sc, _ = ctcbeam_decode_nbest(logprobs, lengths, K, **kw)
     return tok, ln, sc

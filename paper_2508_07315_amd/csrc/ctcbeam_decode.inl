@@ -1101,7 +1101,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     }
   }
 
-  // ---- LM.Final, best beam ----
+  // ---- LM.Final, order of the final hypotheses ----
+  const bool nbest = p.nbest_scores != nullptr;
   if (wave == 0) {
     float s = sc;
     if (HAS_LM && j < K && s != kNegInf) {
@@ -1133,18 +1134,24 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       const float av = alpha * v;
       s = s + av;
     }
-    // argmax, lowest slot on ties
-    float bs = (j < K) ? s : kNegInf;
-    int bj = (j < K) ? j : 0x7FFF;
-    for (int off = 1; off < 64; off <<= 1) {
-      const float os = __shfl_xor(bs, off);
-      const int oj = __shfl_xor(bj, off);
-      if (os > bs || (os == bs && oj < bj)) {
-        bs = os;
-        bj = oj;
-      }
+    // rank of each slot: final score descending, lowest slot on ties
+    const float sj = (j < K) ? s : kNegInf;
+    int rank = 0;
+    for (int i = 0; i < K; ++i) {
+      const float si = rdlane(sj, i);
+      rank += (si > sj || (si == sj && i < j)) ? 1 : 0;
     }
-    const int blen = __shfl(len, bj < 64 ? bj : 0);
+    const uint64_t top = __ballot(j < K && rank == 0);
+    const int bj = static_cast<int>(__builtin_ctzll(top));  // K >= 1: some slot has rank 0
+    const float bs = rdlane(sj, bj);
+    const int blen = rdlane(len, bj);
+    const int nlen = (j < K && sj != kNegInf) ? len : 0;
+    if (nbest && j < K) {
+      p.nbest_scores[static_cast<size_t>(b) * K + rank] = sj;
+      p.nbest_lengths[static_cast<size_t>(b) * K + rank] = nlen;
+      s_row[rank] = static_cast<uint32_t>(nlen);  // lengths by rank (the row table is free now)
+      s_row[kMaxK + j] = static_cast<uint32_t>(rank);
+    }
     if (lane == 0) {
       s_best = bj;
       s_bestscore = bs;
@@ -1165,17 +1172,37 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   const float bscore = s_bestscore;
   const bool have = bscore != kNegInf;
   const int nout = have ? s_bestlen : 0;
-  int32_t* ot = p.out_tokens + static_cast<size_t>(b) * T;
-  for (int tt = nout + tid; tt < T; tt += kThreads) ot[tt] = -1;
-  if (tid == 0) {
+  int32_t* ot = p.out_tokens ? p.out_tokens + static_cast<size_t>(b) * T : nullptr;
+  if (ot)
+    for (int tt = nout + tid; tt < T; tt += kThreads) ot[tt] = -1;
+  if (tid == 0 && p.out_scores) {
     p.out_scores[b] = bscore;
     if (p.out_lengths) p.out_lengths[b] = nout;
   }
+  int32_t* nbt = nbest ? p.nbest_tokens + static_cast<size_t>(b) * K * T : nullptr;
+  if (nbest) {
+    // padding of every row past its transcript
+    for (int r = 0; r < K; ++r) {
+      const int n = static_cast<int>(s_row[r]);
+      for (int tt = n + tid; tt < T; tt += kThreads) nbt[static_cast<size_t>(r) * T + tt] = -1;
+    }
+  }
 
   // ---- traceback through the back-pointers, staged in LDS tiles ----
+  // 1-best: lane 0 of wave 0 walks the best slot.  N-best: lane j of wave 0
+  // walks slot j (every live slot) and writes the row of its rank.
+  // (the LM.Final term is finite, so some slot is live exactly when the best
+  // final score is finite)
+  const bool walker = (wave == 0) && (nbest ? (j < K && sc != kNegInf) : (lane == 0 && have));
   if (have && L > 0) {
     const int tile_frames = kBigWords / K;
-    int jb = best, cnext = -1, pos = nout;
+    int jb = nbest ? j : best, cnext = -1;
+    int32_t* orow = nullptr;
+    int pos = 0;
+    if (walker) {
+      orow = nbest ? nbt + static_cast<size_t>(s_row[kMaxK + j]) * T : ot;
+      pos = nbest ? len : nout;
+    }
     for (int hi = L; hi > 0;) {
       const int lo = hi > tile_frames ? hi - tile_frames : 0;
       __syncthreads();
@@ -1183,13 +1210,16 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       const int32_t* src = bpb + static_cast<size_t>(lo) * K;
       for (int q = tid; q < n; q += kThreads) s_big[q] = static_cast<uint32_t>(src[q]);
       __syncthreads();
-      if (tid == 0) {
+      if (walker) {
         for (int tt = hi - 1; tt >= lo; --tt) {
           const uint32_t e = s_big[(tt - lo) * K + jb];
           const int cl = static_cast<int>(e & 0xFFFFu);
           const int par = static_cast<int>(e >> 16);
           if (tt < L - 1 && cnext != V && cnext != cl) {
-            if (pos > 0) ot[--pos] = cnext;
+            if (pos > 0) {
+              --pos;
+              if (orow) orow[pos] = cnext;
+            }
           }
           cnext = cl;
           jb = par;
@@ -1197,10 +1227,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       }
       hi = lo;
     }
-    if (tid == 0) {
-      if (cnext != V && cnext >= 0 && pos > 0) ot[--pos] = cnext;
-      if (pos != 0) status |= 2u;
+    if (walker) {
+      if (cnext != V && cnext >= 0 && pos > 0) {
+        --pos;
+        if (orow) orow[pos] = cnext;
+      }
     }
+    if (wave == 0 && __ballot(walker && pos != 0) != 0ull) status |= 2u;
   }
   if (tid == 0) p.status[b] = status;
 }

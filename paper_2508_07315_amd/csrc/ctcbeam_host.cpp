@@ -612,10 +612,16 @@ size_t ctcbeam_workspace_bytes(int B, int T, int K) {
   return status_bytes(B) + static_cast<size_t>(B) * static_cast<size_t>(T) * static_cast<size_t>(K) * sizeof(int32_t);
 }
 
-int ctcbeam_decode_ex(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K, float alpha,
-                      float beta, float boost_w, const ctcbeam_lm* lm, const ctcbeam_boost* boost, void* workspace,
-                      size_t workspace_bytes, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
-                      hipStream_t stream, const ctcbeam_opts* opts) {
+namespace {
+
+// Shared body of the decode entry points: validation, parameter block and
+// launch.  Exactly one output set is given: the 1-best (out_*) or the N-best
+// (nbest_*).
+int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K, float alpha,
+                float beta, float boost_w, const ctcbeam_lm* lm, const ctcbeam_boost* boost, void* workspace,
+                size_t workspace_bytes, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
+                int32_t* nbest_tokens, int32_t* nbest_lengths, float* nbest_scores, bool want_nbest,
+                hipStream_t stream, const ctcbeam_opts* opts) {
   if (B < 0 || T < 0) return fail(1, "B and T must be >= 0");
   if (V < 1) return fail(1, "V must be >= 1");
   if (V > CTCBEAM_MAX_V) return fail(2, "V above " + std::to_string(CTCBEAM_MAX_V));
@@ -630,8 +636,10 @@ int ctcbeam_decode_ex(const float* logprobs, const int32_t* lengths, int B, int 
   if (std::isnan(theta) || theta < 0.0f) return fail(1, "prune_theta must be >= 0 (or +inf)");
   if (std::isnan(alpha) || std::isnan(beta) || std::isnan(boost_w)) return fail(1, "NaN weight");
   if (B == 0) return 0;
-  if (!lengths || !out_scores || !workspace || (T > 0 && (!logprobs || !out_tokens)))
-    return fail(1, "null device pointer");
+  if (!lengths || !workspace || (T > 0 && !logprobs)) return fail(1, "null device pointer");
+  if (want_nbest ? (!nbest_lengths || !nbest_scores || (T > 0 && !nbest_tokens))
+                 : (!out_scores || (T > 0 && !out_tokens)))
+    return fail(1, "null output pointer");
   if (workspace_bytes < ctcbeam_workspace_bytes(B, T, K)) return fail(1, "workspace too small");
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return fail(4, "no HIP device");
@@ -662,13 +670,37 @@ int ctcbeam_decode_ex(const float* logprobs, const int32_t* lengths, int B, int 
   }
   p.status = static_cast<uint32_t*>(workspace);
   p.bp = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + status_bytes(B));
-  p.out_tokens = out_tokens;
-  p.out_lengths = out_lengths;
-  p.out_scores = out_scores;
+  if (want_nbest) {
+    p.nbest_tokens = nbest_tokens;  // may be null when T = 0 (empty rows)
+    p.nbest_lengths = nbest_lengths;
+    p.nbest_scores = nbest_scores;
+  } else {
+    p.out_tokens = out_tokens;
+    p.out_lengths = out_lengths;
+    p.out_scores = out_scores;
+  }
   p.stats = opts ? opts->stats : nullptr;
   hipError_t e = ctcbeam::launch_decode(p, stream);
   if (e != hipSuccess) return fail(4, std::string("kernel launch: ") + hipGetErrorString(e));
   return 0;
+}
+
+}  // namespace
+
+int ctcbeam_decode_ex(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K, float alpha,
+                      float beta, float boost_w, const ctcbeam_lm* lm, const ctcbeam_boost* boost, void* workspace,
+                      size_t workspace_bytes, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
+                      hipStream_t stream, const ctcbeam_opts* opts) {
+  return decode_impl(logprobs, lengths, B, T, V, K, alpha, beta, boost_w, lm, boost, workspace, workspace_bytes,
+                     out_tokens, out_lengths, out_scores, nullptr, nullptr, nullptr, false, stream, opts);
+}
+
+int ctcbeam_decode_nbest(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K, float alpha,
+                         float beta, float boost_w, const ctcbeam_lm* lm, const ctcbeam_boost* boost,
+                         void* workspace, size_t workspace_bytes, int32_t* nbest_tokens, int32_t* nbest_lengths,
+                         float* nbest_scores, hipStream_t stream, const ctcbeam_opts* opts) {
+  return decode_impl(logprobs, lengths, B, T, V, K, alpha, beta, boost_w, lm, boost, workspace, workspace_bytes,
+                     nullptr, nullptr, nullptr, nbest_tokens, nbest_lengths, nbest_scores, true, stream, opts);
 }
 
 int ctcbeam_decode(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K, float alpha,

@@ -59,10 +59,16 @@ struct KernelParams {
   // workspace / outputs
   uint32_t* status;          // [B]
   int32_t* bp;               // [B, T, K]
-  int32_t* out_tokens;       // [B, T]
+  int32_t* out_tokens;       // [B, T] or null (then no 1-best output)
   int32_t* out_lengths;      // [B] or null
-  float* out_scores;         // [B]
+  float* out_scores;         // [B] or null
   int64_t* stats;            // [B, 8] or null
+  // N-best output (nbest_scores null: none; nbest_tokens may be null when
+  // T = 0): every slot's final hypothesis ordered by
+  // final score, lowest slot on ties; dead slots last, empty, -inf
+  int32_t* nbest_tokens;     // [B, K, T]
+  int32_t* nbest_lengths;    // [B, K]
+  float* nbest_scores;       // [B, K]
 };
 
 // Kernel variants by labels per lane (V <= 512 * LPT); each dispatches on the

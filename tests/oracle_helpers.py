@@ -96,3 +96,16 @@ def transcripts_from_trace(bp_index, W, t, K):
         labels.reverse()
         res.append((tuple(collapse(labels, V)), labels[-1]))
     return res
+
+
+def brute_force_keys(D, V, **kw):
+    """Best fp32 fold over all (V+1)^T alignments for every recombination key
+    (collapsed transcript, ends-in-blank flag): {key: best score}."""
+    T = D.shape[0]
+    best = {}
+    for align in itertools.product(range(V + 1), repeat=T):
+        s, y = fold_alignment(D, align, V, **kw)
+        key = (tuple(y), (align[-1] if T else V) == V)
+        if key not in best or s > best[key]:
+            best[key] = s
+    return best
