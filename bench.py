@@ -189,6 +189,7 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic},
         "kernel_ms_mean": mean_ms,
+        "kernel_ms_median": float(np.median(k_ms)),
         "kernel_ms_min": float(np.min(k_ms)),
         "algorithmic_bytes_per_launch": alg_bytes,
         "valid_frames_per_s": float(np.sum(lens)) / (mean_ms * 1e-3),
