@@ -18,6 +18,13 @@ Prints ONE JSON line:
                output bytes.
   cpu_baseline = the CPU oracle timed on a bounded sample of the same
                workload (a reported baseline, not a target).
+
+--mode nbest times the N-best entry point on the same workload (all K final
+hypotheses out); --mode greedy times greedy decoding with the same LM fusion
+(Algorithm 1 with one hypothesis; no back-pointers, LM / boosting rows
+rebuilt once per emitted token, so its byte model counts one chain read per
+emission instead of one per live beam-frame).  --batch overrides B (the
+utterances are drawn from the same recipe).
 """
 from __future__ import annotations
 
@@ -26,6 +33,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -35,18 +43,25 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "decoded frames/sec (B×T/s) at K=8, V=1024 + 3-gram LM; % HBM roofline"
+METRIC_BY_MODE = {
+    "beam": METRIC,
+    "nbest": "decoded frames/sec (B×T/s), N-best output, K=8, V=1024 + 3-gram LM; % HBM roofline",
+    "greedy": "decoded frames/sec (B×T/s), greedy + fusion, V=1024 + 3-gram LM; % HBM roofline",
+}
+KERNEL_SOURCES = {"beam": "ctcbeam_decode.inl", "nbest": "ctcbeam_decode.inl", "greedy": "ctcbeam_greedy.inl"}
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(mode: str = "beam") -> str:
     h = hashlib.sha256()
-    for f in ("ctcbeam_decode.inl", "ctcbeam_internal.h"):
+    for f in (KERNEL_SOURCES[mode], "ctcbeam_internal.h"):
         with open(os.path.join(ROOT, "paper_2508_07315_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(stats, B: int, T: int, V: int, K: int) -> int:
-    """Bytes the method must move for one launch (see module docstring)."""
+def algorithmic_bytes(stats, B: int, T: int, V: int, K: int, mode: str = "beam") -> int:
+    """Bytes the method must move for one launch (see module docstring).
+    K = 0 for greedy decoding (no back-pointers)."""
     W = V + 1
     s = stats.astype("int64")
     frames = int(s[:, 0].sum())
@@ -54,11 +69,12 @@ def algorithmic_bytes(stats, B: int, T: int, V: int, K: int) -> int:
     chains = 12 * int(s[:, 2].sum()) + 6 * int(s[:, 3].sum()) + 12 * int(s[:, 4].sum()) + \
         6 * int(s[:, 5].sum())
     emit = 4 * int(s[:, 6].sum())
-    per_utt = B * (8 * V + 4 * T + 4)
+    outputs = K * (4 * T + 8) if mode == "nbest" else 4 * T + 4
+    per_utt = B * (8 * V + outputs)
     return per_frame + chains + emit + per_utt
 
 
-def load_traffic(workload: str):
+def load_traffic(workload: str, mode: str = "beam"):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
     taken on the current kernel source."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
@@ -66,12 +82,12 @@ def load_traffic(workload: str):
         return None
     with open(path) as f:
         d = json.load(f)
-    if d.get("kernel_sha") != kernel_source_hash():
+    if d.get("kernel_sha") != kernel_source_hash(mode):
         return None
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, lp, lens, n_utts: int, threads: int):
+def cpu_baseline(w, lp, lens, n_utts: int, threads: int, mode: str = "beam"):
     import numpy as np
 
     import oracle
@@ -83,8 +99,8 @@ def cpu_baseline(w, lp, lens, n_utts: int, threads: int):
         off, tok = W.phrases_for(w.boost, w.V)
         bt = oracle.BT(w.V, off, tok)
     t0 = time.perf_counter()
-    oracle.decode(lp[idx], lens[idx], w.K, w.alpha, w.beta, w.boost_w, theta=w.theta, lm=lm, bt=bt,
-                  n_threads=threads)
+    oracle.decode(lp[idx], lens[idx], 1 if mode == "greedy" else w.K, w.alpha, w.beta, w.boost_w,
+                  theta=w.theta, lm=lm, bt=bt, n_threads=threads, want_nbest=mode == "nbest")
     dt = time.perf_counter() - t0
     frames = len(idx) * w.T
     return dict(value=frames / dt, unit="frames/s", cores=min(threads, len(idx)), kind="oracle",
@@ -99,6 +115,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3, help="workload 1..5 (default 3)")
+    ap.add_argument("--mode", choices=("beam", "nbest", "greedy"), default="beam")
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's B")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-utts", type=int, default=8)
     ap.add_argument("--cpu-threads", type=int, default=8)
@@ -120,6 +138,8 @@ def main():
     P._load()  # no CPU fallback: fails loudly if the HIP library is missing
     dev = torch.device("cuda:0")
     w = W.CONFIGS[args.config]
+    if args.batch > 0 and args.batch != w.B:
+        w = w.replace(B=args.batch, name=re.sub(r"_B\d+_", f"_B{args.batch}_", w.name))
     t_setup = time.perf_counter()
     lens = W.make_lengths(w)
     lp = W.make_logprobs(w)
@@ -138,14 +158,27 @@ def main():
     stats = torch.zeros((B, 8), dtype=torch.int64, device=dev)
     print(f"# setup {time.perf_counter() - t_setup:.1f} s: {w.name}", file=sys.stderr, flush=True)
 
+    mode = args.mode
+    if mode == "nbest":
+        nb_tok = torch.empty((B, K, T), dtype=torch.int32, device=dev)
+        nb_len = torch.empty((B, K), dtype=torch.int32, device=dev)
+        nb_sc = torch.empty((B, K), dtype=torch.float32, device=dev)
+
     def launch(st=None):
-        P.ctcbeam_decode_ex(d_lp, d_len, K, w.alpha, w.beta, w.boost_w, lm, bt, ws, out_tok,
-                            out_len, out_sc, theta=w.theta, stats=st)
+        if mode == "beam":
+            P.ctcbeam_decode_ex(d_lp, d_len, K, w.alpha, w.beta, w.boost_w, lm, bt, ws, out_tok,
+                                out_len, out_sc, theta=w.theta, stats=st)
+        elif mode == "nbest":
+            P.ctcbeam_decode_nbest(d_lp, d_len, K, w.alpha, w.beta, w.boost_w, lm, bt, ws, nb_tok,
+                                   nb_len, nb_sc, theta=w.theta, stats=st)
+        else:
+            P.ctcbeam_greedy_decode(d_lp, d_len, w.alpha, w.beta, w.boost_w, lm, bt, ws, out_tok,
+                                    out_len, out_sc, stats=st)
 
     # untimed launch with the kernel's counters on: algorithmic bytes
     launch(stats)
     torch.cuda.synchronize()
-    alg_bytes = algorithmic_bytes(stats.cpu().numpy(), B, T, V, K)
+    alg_bytes = algorithmic_bytes(stats.cpu().numpy(), B, T, V, 0 if mode == "greedy" else K, mode)
     status = P.ctcbeam_query_status(ws, B)
     for _ in range(args.warmup):
         launch()
@@ -166,9 +199,9 @@ def main():
     ms_per_step = wall * 1e3 / args.steps
     value = B * T / (mean_ms * 1e-3)
     achieved = alg_bytes / (mean_ms * 1e-3) / 1e9
-    traffic = load_traffic(w.name)
+    traffic = load_traffic(w.name if mode == "beam" else f"{w.name}_{mode}", mode)
     result = {
-        "metric": METRIC,
+        "metric": METRIC_BY_MODE[mode],
         "value": value,
         "unit": "frames/s",
         "n_gpus": 1,
@@ -180,11 +213,12 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "B": B, "T": T, "V": V, "K": K,
+        "config": {"workload": w.name, "mode": mode, "B": B, "T": T, "V": V, "K": 1 if mode == "greedy" else K,
                    "lm": None if w.lm is None else f"{w.lm.order}-gram, {'/'.join(str(c) for c in w.lm.counts)} explicit n-grams",
                    "boost": None if w.boost is None else f"{w.boost.n_phrases} phrases",
                    "alpha": w.alpha, "beta": w.beta, "boost_w": w.boost_w, "theta": w.theta,
-                   "parallelism": "one workgroup per utterance"},
+                   "parallelism": "one wave per utterance" if mode == "greedy"
+                   else "one workgroup per utterance"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic},
@@ -206,7 +240,7 @@ def main():
         result["copy_calibration_bytes"] = n * 4
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, lp, lens, args.cpu_utts,
-                                              max(1, min(args.cpu_threads, os.cpu_count() or 1)))
+                                              max(1, min(args.cpu_threads, os.cpu_count() or 1)), mode)
     print(json.dumps(result), flush=True)
 
 

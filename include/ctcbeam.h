@@ -189,6 +189,31 @@ int ctcbeam_decode_nbest(const float* logprobs, const int32_t* lengths, int B, i
                          int32_t* nbest_tokens, int32_t* nbest_lengths, float* nbest_scores,
                          hipStream_t stream, const ctcbeam_opts* opts);
 
+/*
+ * Greedy decoding with LM shallow fusion and phrase boosting: Algorithm 1
+ * with a single hypothesis (the greedy rows with LM / PB customisation of
+ * Table II, Sec. V-A).  At every frame the hypothesis takes the label
+ * with the best Eq. 1 score (same fp32 fold and tie order as the beam search;
+ * pruning and recombination have no effect with one hypothesis), then
+ * LM.Final.  Results equal ctcbeam_decode_ex with K = 1.
+ *   logprobs, lengths, B, T, V, alpha, beta, boost_w, lm, boost, out_* :
+ *                  as for ctcbeam_decode (out_lengths may be NULL)
+ *   workspace    : device buffer of at least ctcbeam_workspace_bytes(B, 0, 1)
+ *                  bytes (only the per-utterance status words are used; a
+ *                  workspace sized for a beam decode of the same B fits)
+ *   opts         : may be NULL; prune_theta is ignored; stats, when given,
+ *                  receives per utterance {frames, live frames, LM chain
+ *                  states read, LM arcs read, boosting chain nodes, boosting
+ *                  arcs, emitted tokens, state refills}
+ * One kernel launch on `stream`, one wave per utterance, no allocation.
+ * Errors as for ctcbeam_decode_ex.
+ */
+int ctcbeam_greedy_decode(const float* logprobs, const int32_t* lengths, int B, int T, int V,
+                          float alpha, float beta, float boost_w, const ctcbeam_lm* lm,
+                          const ctcbeam_boost* boost, void* workspace, size_t workspace_bytes,
+                          int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
+                          hipStream_t stream, const ctcbeam_opts* opts);
+
 /* Status bits of the last decode that used `workspace` (synchronises
  * `stream`): bit 0 = a length was clamped, bit 1 = internal traceback
  * mismatch, bit 2 = internal staging overflow. */

@@ -78,6 +78,8 @@ def _load():
     lib.ctcbeam_decode_ex.argtypes = dec + [P]
     lib.ctcbeam_decode_nbest.restype = I
     lib.ctcbeam_decode_nbest.argtypes = dec + [P]
+    lib.ctcbeam_greedy_decode.restype = I
+    lib.ctcbeam_greedy_decode.argtypes = [P, P, I, I, I, F, F, F, P, P, P, ctypes.c_size_t, P, P, P, P, P]
     lib.ctcbeam_query_status.restype = I
     lib.ctcbeam_query_status.argtypes = [P, I, P, ctypes.POINTER(ctypes.c_uint32)]
     lib.ctcbeam_lm_tables.restype = I
@@ -368,6 +370,49 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
         _dptr(nbest_scores, torch.float32, "nbest_scores", (B, K)), ctypes.c_void_p(stream), opts)
     _check(rc)
     return nbest_tokens, nbest_lengths, nbest_scores, workspace
+
+
+def ctcbeam_greedy_decode(logprobs, lengths, alpha: float = 0.0, beta: float = 0.0,
+                          boost_w: float = 0.0, lm: Optional[LM] = None,
+                          boost: Optional[Boost] = None, workspace=None, out_tokens=None,
+                          out_lengths=None, out_scores=None, stream=None, stats=None):
+    """Enqueue one greedy decode with fusion (Algorithm 1 with one hypothesis)
+    on ``stream``.  Returns (tokens [B,T] int32 with -1 padding, lengths [B],
+    scores [B], workspace uint8)."""
+    import torch
+    lib = _load()
+    if logprobs.dim() != 3:
+        raise ValueError("logprobs must be [B, T, V+1]")
+    B, T, W = (int(x) for x in logprobs.shape)
+    V = W - 1
+    dev = logprobs.device
+    if out_tokens is None:
+        out_tokens = torch.empty((B, T), dtype=torch.int32, device=dev)
+    if out_lengths is None:
+        out_lengths = torch.empty((B,), dtype=torch.int32, device=dev)
+    if out_scores is None:
+        out_scores = torch.empty((B,), dtype=torch.float32, device=dev)
+    need = ctcbeam_workspace_bytes(B, 0, 1)
+    if workspace is None:
+        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
+    ws = _dptr(workspace, torch.uint8, "workspace")
+    opts = None
+    if stats is not None:
+        o = _Opts()
+        o.prune_theta = math.inf
+        o.stats = _dptr(stats, torch.int64, "stats", (B, 8)).value
+        opts = ctypes.byref(o)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev).cuda_stream
+    rc = lib.ctcbeam_greedy_decode(
+        _dptr(logprobs, torch.float32, "logprobs"), _dptr(lengths, torch.int32, "lengths", (B,)),
+        B, T, V, float(alpha), float(beta), float(boost_w),
+        lm.handle if lm is not None else None, boost.handle if boost is not None else None,
+        ws, int(workspace.numel()), _dptr(out_tokens, torch.int32, "out_tokens", (B, T)),
+        _dptr(out_lengths, torch.int32, "out_lengths", (B,)),
+        _dptr(out_scores, torch.float32, "out_scores", (B,)), ctypes.c_void_p(stream), opts)
+    _check(rc)
+    return out_tokens, out_lengths, out_scores, workspace
 
 
 def ctcbeam_query_status(workspace, B: int, stream=None) -> int:

@@ -621,7 +621,7 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
                 float beta, float boost_w, const ctcbeam_lm* lm, const ctcbeam_boost* boost, void* workspace,
                 size_t workspace_bytes, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
                 int32_t* nbest_tokens, int32_t* nbest_lengths, float* nbest_scores, bool want_nbest,
-                hipStream_t stream, const ctcbeam_opts* opts) {
+                bool greedy, hipStream_t stream, const ctcbeam_opts* opts) {
   if (B < 0 || T < 0) return fail(1, "B and T must be >= 0");
   if (V < 1) return fail(1, "V must be >= 1");
   if (V > CTCBEAM_MAX_V) return fail(2, "V above " + std::to_string(CTCBEAM_MAX_V));
@@ -632,7 +632,7 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
   if (boost && boost->V != V) return fail(1, "boosting tree vocabulary size differs from V");
   if (lm && !lm->d_arcs) return fail(1, "LM handle has no device tables (host-only build)");
   if (boost && !boost->d_nodes) return fail(1, "boosting handle has no device tables (host-only build)");
-  const float theta = opts ? opts->prune_theta : std::numeric_limits<float>::infinity();
+  const float theta = (opts && !greedy) ? opts->prune_theta : std::numeric_limits<float>::infinity();
   if (std::isnan(theta) || theta < 0.0f) return fail(1, "prune_theta must be >= 0 (or +inf)");
   if (std::isnan(alpha) || std::isnan(beta) || std::isnan(boost_w)) return fail(1, "NaN weight");
   if (B == 0) return 0;
@@ -640,7 +640,7 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
   if (want_nbest ? (!nbest_lengths || !nbest_scores || (T > 0 && !nbest_tokens))
                  : (!out_scores || (T > 0 && !out_tokens)))
     return fail(1, "null output pointer");
-  if (workspace_bytes < ctcbeam_workspace_bytes(B, T, K)) return fail(1, "workspace too small");
+  if (workspace_bytes < ctcbeam_workspace_bytes(B, greedy ? 0 : T, K)) return fail(1, "workspace too small");
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess) return fail(4, "no HIP device");
   if (lm && lm->device != dev) return fail(1, "LM tables live on another device");
@@ -680,7 +680,7 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
     p.out_scores = out_scores;
   }
   p.stats = opts ? opts->stats : nullptr;
-  hipError_t e = ctcbeam::launch_decode(p, stream);
+  hipError_t e = greedy ? ctcbeam::launch_greedy(p, stream) : ctcbeam::launch_decode(p, stream);
   if (e != hipSuccess) return fail(4, std::string("kernel launch: ") + hipGetErrorString(e));
   return 0;
 }
@@ -692,7 +692,7 @@ int ctcbeam_decode_ex(const float* logprobs, const int32_t* lengths, int B, int 
                       size_t workspace_bytes, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
                       hipStream_t stream, const ctcbeam_opts* opts) {
   return decode_impl(logprobs, lengths, B, T, V, K, alpha, beta, boost_w, lm, boost, workspace, workspace_bytes,
-                     out_tokens, out_lengths, out_scores, nullptr, nullptr, nullptr, false, stream, opts);
+                     out_tokens, out_lengths, out_scores, nullptr, nullptr, nullptr, false, false, stream, opts);
 }
 
 int ctcbeam_decode_nbest(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K, float alpha,
@@ -700,7 +700,15 @@ int ctcbeam_decode_nbest(const float* logprobs, const int32_t* lengths, int B, i
                          void* workspace, size_t workspace_bytes, int32_t* nbest_tokens, int32_t* nbest_lengths,
                          float* nbest_scores, hipStream_t stream, const ctcbeam_opts* opts) {
   return decode_impl(logprobs, lengths, B, T, V, K, alpha, beta, boost_w, lm, boost, workspace, workspace_bytes,
-                     nullptr, nullptr, nullptr, nbest_tokens, nbest_lengths, nbest_scores, true, stream, opts);
+                     nullptr, nullptr, nullptr, nbest_tokens, nbest_lengths, nbest_scores, true, false, stream, opts);
+}
+
+int ctcbeam_greedy_decode(const float* logprobs, const int32_t* lengths, int B, int T, int V, float alpha,
+                          float beta, float boost_w, const ctcbeam_lm* lm, const ctcbeam_boost* boost,
+                          void* workspace, size_t workspace_bytes, int32_t* out_tokens, int32_t* out_lengths,
+                          float* out_scores, hipStream_t stream, const ctcbeam_opts* opts) {
+  return decode_impl(logprobs, lengths, B, T, V, 1, alpha, beta, boost_w, lm, boost, workspace, workspace_bytes,
+                     out_tokens, out_lengths, out_scores, nullptr, nullptr, nullptr, false, true, stream, opts);
 }
 
 int ctcbeam_decode(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K, float alpha,

@@ -78,6 +78,19 @@ hipError_t launch_lpt2(const KernelParams& p, hipStream_t stream);
 hipError_t launch_lpt4(const KernelParams& p, hipStream_t stream);
 hipError_t launch_lpt8(const KernelParams& p, hipStream_t stream);
 
+// Greedy (one hypothesis) kernels by labels per lane: up to 256, 1024 and
+// 4096 tokens.
+hipError_t launch_greedy_nj4(const KernelParams& p, hipStream_t stream);
+hipError_t launch_greedy_nj16(const KernelParams& p, hipStream_t stream);
+hipError_t launch_greedy_nj64(const KernelParams& p, hipStream_t stream);
+
+inline hipError_t launch_greedy(const KernelParams& p, hipStream_t stream) {
+  if (p.B == 0) return hipSuccess;
+  if (p.V <= 256) return launch_greedy_nj4(p, stream);
+  if (p.V <= 1024) return launch_greedy_nj16(p, stream);
+  return launch_greedy_nj64(p, stream);
+}
+
 inline hipError_t launch_decode(const KernelParams& p, hipStream_t stream) {
   if (p.B == 0) return hipSuccess;
   if (p.V <= 512) return launch_lpt1(p, stream);

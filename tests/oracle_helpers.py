@@ -81,6 +81,41 @@ def greedy(D, L, V):
     return collapse(align, V), s
 
 
+def greedy_fused(D, L, V, alpha=0.0, beta=0.0, boost_w=0.0, lm=None, bt=None):
+    """Greedy decoding with fusion written as its own sequential search: at
+    every frame score each label with the candidate fold of Eq. 1 (the same
+    steps as fold_alignment), keep the first maximum (lowest label), then
+    LM.Final.  A frame whose best candidate is -inf ends the hypothesis
+    (empty transcript, -inf).  Returns (transcript, score)."""
+    s = F32(0.0)
+    last = V
+    y, q = [], []
+    for t in range(L):
+        best, arg, arg_q = NEG_INF, -1, None
+        for c in range(V + 1):
+            x = F32(s + F32(D[t, c]))
+            q2 = q
+            if c != V and c != last:
+                x = F32(x + F32(beta))
+                if lm is not None:
+                    x = F32(x + F32(F32(alpha) * F32(lm.score(y, c))))
+                if bt is not None:
+                    sc, q2 = bt.step(q, c)
+                    x = F32(x + F32(F32(boost_w) * F32(sc)))
+            if x > best:
+                best, arg, arg_q = x, c, q2
+        if best == NEG_INF:
+            return [], NEG_INF
+        if arg != V and arg != last:
+            y.append(arg)
+            q = arg_q
+        last = arg
+        s = best
+    if lm is not None:
+        s = F32(s + F32(F32(alpha) * F32(lm.score(y, V))))
+    return y, s
+
+
 def transcripts_from_trace(bp_index, W, t, K):
     """Collapsed transcript and last label of every slot after frame t,
     rebuilt by walking the backpointers."""
