@@ -77,20 +77,32 @@ __device__ __forceinline__ int wave_min(int v) {
   return min(min(a, b), min(c, d));
 }
 
+// four consecutive fp32 at a 4-byte aligned address (one dwordx4 access)
+typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));
+typedef float f4a __attribute__((ext_vector_type(4), aligned(16)));
+
+// Label of a lane's r-th slot: lanes own runs of 4 consecutive labels, runs of
+// the wave are 256 labels apart, so a frame row is read with dwordx4 loads
+// and the LDS arrays with 16-byte accesses.
+__device__ __forceinline__ int label_of(int lane, int r) { return 256 * (r >> 2) + 4 * lane + (r & 3); }
+// the lane that owns label c
+__device__ __forceinline__ int lane_of(int c) { return (c >> 2) & 63; }
+
 template <int NJ, int NLEV, bool HAS_BT>
 __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
+  static_assert(NJ % 4 == 0, "labels per lane come in runs of 4");
   constexpr bool HAS_LM = NLEV >= 0;
   constexpr int NL = NLEV > 0 ? NLEV : 0;  // chain levels above the unigram root
   constexpr int NLA = NL > 0 ? NL : 1;
   constexpr int NCAP = 64 * NJ;            // token capacity
   constexpr int P = 64 / NJ;               // frames per prefetch batch
   // per-label fusion terms of the current state, and the label's successor
-  __shared__ float s_av[HAS_LM ? NCAP : 1];       // fl(alpha * LM(c | state))
-  __shared__ uint32_t s_tg[HAS_LM ? NCAP : 1];    // LM state after emitting c
-  __shared__ float s_p1[HAS_LM ? NCAP : 1];       // unigram ln P(c)
-  __shared__ float s_bv[HAS_BT ? NCAP : 1];       // fl(w * BT(c | state))
-  __shared__ uint32_t s_bk[HAS_BT ? NCAP : 1];    // boosting key of c
-  __shared__ uint32_t s_root[HAS_BT ? NCAP : 1];  // root keys
+  __shared__ __align__(16) float s_av[HAS_LM ? NCAP : 1];       // fl(alpha * LM(c | state))
+  __shared__ __align__(16) uint32_t s_tg[HAS_LM ? NCAP : 1];    // LM state after emitting c
+  __shared__ __align__(16) float s_p1[HAS_LM ? NCAP : 1];       // unigram ln P(c)
+  __shared__ __align__(16) float s_bv[HAS_BT ? NCAP : 1];       // fl(w * BT(c | state))
+  __shared__ __align__(16) uint32_t s_bk[HAS_BT ? NCAP : 1];    // boosting key of c
+  __shared__ __align__(16) uint32_t s_root[HAS_BT ? NCAP : 1];  // root keys
 
   const int lane = threadIdx.x;
   const int b = blockIdx.x;
@@ -104,7 +116,7 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
 
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
-    const int c = lane + 64 * j;
+    const int c = label_of(lane, j);
     if (HAS_LM) s_p1[c] = c < V ? p.lm_unigram[c] : 0.0f;
     if (HAS_BT) s_root[c] = c < V ? p.bt_root_key[c] : 0u;
   }
@@ -133,7 +145,7 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
       // unigram + backoff fold of every label (innermost context first)
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
-        const int c = lane + 64 * j;
+        const int c = label_of(lane, j);
         float v = s_p1[c];
 #pragma unroll
         for (int l = 0; l < NL; ++l) v = v + hl[l].bo;
@@ -145,7 +157,7 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
       pot = static_cast<int>(nd.pot & 0xFFu);
 #pragma unroll
       for (int j = 0; j < NJ; ++j) {
-        const int c = lane + 64 * j;
+        const int c = label_of(lane, j);
         const uint32_t k = s_root[c];
         s_bk[c] = k;
         s_bv[c] = boost_w * static_cast<float>(static_cast<int>((k >> 20) & 63u) - pot);
@@ -230,7 +242,7 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
     int jb = 0;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
-      const int c = lane + 64 * j;
+      const int c = label_of(lane, j);
       const float x0 = s + d[j];
       float x1 = x0 + beta;
       if (HAS_LM) x1 = x1 + s_av[c];
@@ -251,14 +263,14 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
       xw = xblank;
     } else {
       const uint64_t m = __ballot(xb == g);
-      const int cl = lane + 64 * jb;
+      const int cl = label_of(lane, jb);
       if (__popcll(m) == 1) {
         cw = __builtin_amdgcn_readlane(cl, static_cast<int>(__builtin_ctzll(m)));
       } else {
         cw = wave_min((xb == g) ? cl : 0x7FFFFFFF);
       }
       // the winner's own value (g may differ from it in the sign of a zero)
-      xw = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xb), cw & 63));
+      xw = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(xb), lane_of(cw)));
     }
     if (xw == kNegInf) {
       dead = true;
@@ -296,9 +308,18 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
       if (t0 + f < L) {  // uniform
         const float* row = Db + static_cast<size_t>(t0 + f) * W;
 #pragma unroll
-        for (int j = 0; j < NJ; ++j) {
-          const int c = lane + 64 * j;
-          q[f][j] = c < V ? __builtin_nontemporal_load(row + c) : kNegInf;
+        for (int j = 0; j < NJ; j += 4) {
+          const int c = label_of(lane, j);
+          if (256 * (j >> 2) + 255 < V) {  // uniform: the whole run of the wave is in range
+            const f4u v = __builtin_nontemporal_load(reinterpret_cast<const f4u*>(row + c));
+            q[f][j] = v.x;
+            q[f][j + 1] = v.y;
+            q[f][j + 2] = v.z;
+            q[f][j + 3] = v.w;
+          } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) q[f][j + i] = c + i < V ? __builtin_nontemporal_load(row + c + i) : kNegInf;
+          }
         }
         u[f] = __builtin_nontemporal_load(row + V);
       }
