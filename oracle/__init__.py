@@ -66,7 +66,9 @@ def _load():
     lib.oracle_decode.restype = ctypes.c_int
     lib.oracle_decode.argtypes = [P, P, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                   ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
-                                  P, P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P]
+                                  ctypes.c_int, P, P, ctypes.c_int, P, P, P, P, P, P, P, P, P, P]
+    lib.oracle_lse32.restype = ctypes.c_float
+    lib.oracle_lse32.argtypes = [ctypes.c_float, ctypes.c_float]
     _lib = lib
     return lib
 
@@ -82,6 +84,11 @@ def _ptr(a: Optional[np.ndarray]):
 def _ip(seq):
     arr = _i32(np.asarray(seq, dtype=np.int32).reshape(-1))
     return arr, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def lse32(a: float, b: float) -> np.float32:
+    """The oracle's fp32 log(exp(a) + exp(b)) (log-sum-exp recombination)."""
+    return np.float32(_load().oracle_lse32(float(a), float(b)))
 
 
 class LM:
@@ -164,13 +171,18 @@ class BT:
 def decode(logprobs: np.ndarray, lengths, K: int, alpha: float = 0.0, beta: float = 0.0,
            boost_w: float = 0.0, theta: float = math.inf, lm: Optional[LM] = None,
            bt: Optional[BT] = None, n_threads: int = 1, want_align: bool = False,
-           want_trace: bool = False, want_counters: bool = False, want_nbest: bool = False) -> dict:
+           want_trace: bool = False, want_counters: bool = False, want_nbest: bool = False,
+           logsumexp: bool = False, boost_rollback: bool = False) -> dict:
     """Run the oracle on host arrays.  logprobs: fp32 [B, T, V+1] (blank = V).
 
     want_nbest adds every slot's final hypothesis ordered by final score
     (lowest slot on ties; dead slots last, empty, -inf): nbest_tokens
-    [B, K, T] (-1 padded), nbest_lengths [B, K], nbest_scores [B, K]."""
+    [B, K, T] (-1 padded), nbest_lengths [B, K], nbest_scores [B, K].
+    logsumexp merges recombined hypotheses with lse32 instead of max;
+    boost_rollback takes back the pending boosting of unfinished phrases at
+    the end of the utterance."""
     lib = _load()
+    flags = (1 if logsumexp else 0) | (2 if boost_rollback else 0)
     lp = np.ascontiguousarray(logprobs, dtype=np.float32)
     B, T, W = lp.shape
     V = W - 1
@@ -187,7 +199,7 @@ def decode(logprobs: np.ndarray, lengths, K: int, alpha: float = 0.0, beta: floa
     nbl = np.empty((B, K), dtype=np.int32) if want_nbest else None
     nbs = np.empty((B, K), dtype=np.float32) if want_nbest else None
     rc = lib.oracle_decode(_ptr(lp), _ptr(ln), B, T, V, int(K), float(alpha), float(beta),
-                           float(boost_w), float(theta), lm._h if lm else None,
+                           float(boost_w), float(theta), int(flags), lm._h if lm else None,
                            bt._h if bt else None, int(n_threads), _ptr(toks), _ptr(lens),
                            _ptr(scores), _ptr(align), _ptr(bp), _ptr(ss), _ptr(cnt),
                            _ptr(nbt), _ptr(nbl), _ptr(nbs))

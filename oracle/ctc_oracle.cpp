@@ -27,6 +27,12 @@
 //     both or neither end in blank; the lower slot (higher score) survives
 //     with its own score (max, Viterbi) and dead slots stay in place;
 //   * final: alive scores get fl(alpha * LM(k, </s>)) (Alg. 1, LM.Final);
+//   * variants (flags; Sec. III-C leaves them open): bit 0 merges recombined
+//     hypotheses by log-sum-exp instead of max -- the surviving lower slot
+//     takes lse32(own, other) for each later duplicate in slot order, which
+//     sums the probability of all alignments of a transcript; bit 1 rolls
+//     back the pending boosting of an unfinished phrase at the end of the
+//     utterance: after LM.Final, alive scores get fl(w * -pot(q));
 //   * output: best slot, lowest index on ties; if its score is -inf the
 //     transcript is empty and the score -inf;
 //   * N-best output (all K final hypotheses, the batched-hypotheses result of
@@ -63,6 +69,7 @@
 #include <string>
 #include <thread>
 #include <unordered_map>
+#include <utility>
 #include <vector>
 
 namespace {
@@ -197,11 +204,71 @@ struct Cand {
   int64_t i;
 };
 
+// ---- fp32 log-sum-exp, every step an IEEE fp32 operation in a fixed order
+// (so that any implementation following the same steps gets the same bits).
+// exp: Cody-Waite reduction d = k ln2 + r, k = rint(d / ln2), |r| <= ln2/2,
+// with ln2 split into a 9-bit head (k * head exact) and a tail, then the
+// degree-7 Taylor polynomial of e^r by Horner, scaled by 2^k.  Valid for
+// -80 <= d <= 0 (2^k stays a normal number).
+float exp32_nonpos(float d) {
+  const float inv_ln2 = 1.44269504f;
+  const float ln2_hi = 0.693359375f;
+  const float ln2_lo = -2.12194440e-4f;
+  const float k = std::nearbyint(d * inv_ln2);
+  const float r = (d - k * ln2_hi) - k * ln2_lo;
+  float p = 1.0f / 5040.0f;
+  p = p * r + 1.0f / 720.0f;
+  p = p * r + 1.0f / 120.0f;
+  p = p * r + 1.0f / 24.0f;
+  p = p * r + 1.0f / 6.0f;
+  p = p * r + 0.5f;
+  p = p * r + 1.0f;
+  p = p * r + 1.0f;
+  const int ki = static_cast<int>(k);
+  uint32_t bits = static_cast<uint32_t>(ki + 127) << 23;
+  float scale;
+  std::memcpy(&scale, &bits, sizeof(scale));
+  return p * scale;
+}
+
+// log(1 + e) for 2^-24 <= e <= 1: with s = e / (2 + e), log(1 + e) =
+// 2 atanh(s) = 2 s (1 + s^2/3 + s^4/5 + ... + s^16/17), s <= 1/3.
+float log1p32_unit(float e) {
+  const float s = e / (2.0f + e);
+  const float z = s * s;
+  float q = 1.0f / 17.0f;
+  q = q * z + 1.0f / 15.0f;
+  q = q * z + 1.0f / 13.0f;
+  q = q * z + 1.0f / 11.0f;
+  q = q * z + 1.0f / 9.0f;
+  q = q * z + 1.0f / 7.0f;
+  q = q * z + 1.0f / 5.0f;
+  q = q * z + 1.0f / 3.0f;
+  q = q * z + 1.0f;
+  const float t = s * q;
+  return t + t;
+}
+
+// log(exp(a) + exp(b)) in fp32.
+float lse32(float a, float b) {
+  if (a < b) std::swap(a, b);
+  if (b == NEG_INF) return a;
+  const float d = b - a;
+  if (d < -80.0f) return a;
+  const float e = exp32_nonpos(d);
+  const float l = (e < 5.9604645e-8f) ? e : log1p32_unit(e);
+  return a + l;
+}
+
+constexpr int kFlagLogSumExp = 1;
+constexpr int kFlagBoostRollback = 2;
+
 struct DecodeArgs {
   const float* logprobs;
   const int32_t* lengths;
   int B, T, V, K;
   float alpha, beta, boost_w, theta;
+  int flags;
   const OracleLM* lm;
   const OracleBT* bt;
   int32_t* out_tokens;
@@ -299,12 +366,14 @@ void decode_one(const DecodeArgs& a, int b) {
       frame_parent[t][j] = p;
       frame_label[t][j] = c;
     }
-    // Recombination: same collapsed transcript and same ends-in-blank flag.
+    // Recombination: same collapsed transcript and same ends-in-blank flag;
+    // the first live slot of a transcript absorbs the later ones.
     for (int j = 1; j < K; ++j) {
       if (nh[j].s == NEG_INF) continue;
       for (int i = 0; i < j; ++i) {
         if (nh[i].s == NEG_INF) continue;
         if (nh[i].y == nh[j].y && ((nh[i].last == V) == (nh[j].last == V))) {
+          if (a.flags & kFlagLogSumExp) nh[i].s = lse32(nh[i].s, nh[j].s);
           nh[j].s = NEG_INF;
           break;
         }
@@ -326,6 +395,14 @@ void decode_one(const DecodeArgs& a, int b) {
       float l = a.lm->score(hyp[k].y, V);
       float al = a.alpha * l;
       hyp[k].s = hyp[k].s + al;
+    }
+  }
+  // End-of-utterance rollback of pending boosting (variant flag).
+  if (a.bt && (a.flags & kFlagBoostRollback)) {
+    for (int k = 0; k < K; ++k) {
+      if (hyp[k].s == NEG_INF) continue;
+      float wb = a.boost_w * static_cast<float>(-a.bt->pot(hyp[k].q));
+      hyp[k].s = hyp[k].s + wb;
     }
   }
   int best = 0;
@@ -471,15 +548,19 @@ int oracle_bt_pot(const void* bt, const int32_t* q, int nq) {
   return p->pot(std::vector<int32_t>(q, q + nq));
 }
 
+// fp32 log-sum-exp of the recombination variant (for its pins).
+float oracle_lse32(float a, float b) { return lse32(a, b); }
+
 // Batched beam search over host arrays (same argument meaning as the device
 // decoder; theta = +inf disables pruning).  n_threads > 1 spreads utterances
 // over std::threads.  Optional outputs (null to skip): the best path's frame
 // labels, per-frame back-pointer indices and slot scores, work counters, and
-// the N-best list (tokens [B,K,T], lengths [B,K], scores [B,K]).  Returns 0 on
-// success, 1 on invalid arguments.
+// the N-best list (tokens [B,K,T], lengths [B,K], scores [B,K]).  flags: bit 0
+// log-sum-exp recombination, bit 1 end-of-utterance boosting rollback.
+// Returns 0 on success, 1 on invalid arguments.
 int oracle_decode(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K,
-                  float alpha, float beta, float boost_w, float theta, const void* lm, const void* bt,
-                  int n_threads, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
+                  float alpha, float beta, float boost_w, float theta, int flags, const void* lm,
+                  const void* bt, int n_threads, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
                   int32_t* out_align, int32_t* bp_index, float* slot_scores, int64_t* counters,
                   int32_t* nbest_tokens, int32_t* nbest_lengths, float* nbest_scores) {
   if (B < 0 || T < 0 || V < 1 || K < 1 || !out_tokens || !out_scores) return 1;
@@ -489,7 +570,7 @@ int oracle_decode(const float* logprobs, const int32_t* lengths, int B, int T, i
   if (plm && plm->V != V) return 1;
   const OracleBT* pbt = static_cast<const OracleBT*>(bt);
   if (pbt && pbt->V != V) return 1;
-  DecodeArgs a{logprobs, lengths, B, T, V, K, alpha, beta, boost_w, theta, plm, pbt,
+  DecodeArgs a{logprobs, lengths, B, T, V, K, alpha, beta, boost_w, theta, flags, plm, pbt,
                out_tokens, out_lengths, out_scores, out_align, bp_index, slot_scores, counters,
                nbest_tokens, nbest_lengths, nbest_scores};
   if (n_threads <= 1 || B <= 1) {

@@ -26,9 +26,11 @@ def collapse(align, V):
     return out
 
 
-def fold_alignment(D, align, V, alpha=0.0, beta=0.0, boost_w=0.0, lm=None, bt=None):
+def fold_alignment(D, align, V, alpha=0.0, beta=0.0, boost_w=0.0, lm=None, bt=None,
+                   rollback=False):
     """fp32 score of one alignment: the per-frame left fold of the candidate
-    score (Alg. 1 score update, Eq. 1), then LM.Final.  D: [T, V+1] fp32."""
+    score (Alg. 1 score update, Eq. 1), then LM.Final (and, with rollback, the
+    pending boosting taken back).  D: [T, V+1] fp32."""
     s = F32(0.0)
     last = V
     y = []
@@ -50,6 +52,8 @@ def fold_alignment(D, align, V, alpha=0.0, beta=0.0, boost_w=0.0, lm=None, bt=No
         s = x
     if lm is not None:
         s = F32(s + F32(F32(alpha) * F32(lm.score(y, V))))
+    if rollback and bt is not None and s != NEG_INF:
+        s = F32(s + F32(F32(boost_w) * F32(-bt.pot(q))))
     return s, y
 
 
@@ -67,6 +71,25 @@ def brute_force(D, V, **kw):
         elif s == best:
             arg.add(tuple(y))
     return best, arg
+
+
+def brute_force_keys_logsum(D, V, **kw):
+    """For every recombination key (collapsed transcript, ends-in-blank) the
+    log of the summed probability of all its alignments, in fp64 from the
+    fp32 fold of each alignment: {key: log sum exp(fold)}."""
+    T = D.shape[0]
+    acc = {}
+    for align in itertools.product(range(V + 1), repeat=T):
+        s, y = fold_alignment(D, align, V, **kw)
+        if s == NEG_INF:
+            continue
+        key = (tuple(y), (align[-1] if T else V) == V)
+        acc.setdefault(key, []).append(float(s))
+    out = {}
+    for key, v in acc.items():
+        m = max(v)
+        out[key] = m + float(np.log(np.sum(np.exp(np.array(v) - m))))
+    return out
 
 
 def greedy(D, L, V):
