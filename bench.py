@@ -117,6 +117,9 @@ def main():
     ap.add_argument("--config", type=int, default=3, help="workload 1..5 (default 3)")
     ap.add_argument("--mode", choices=("beam", "nbest", "greedy"), default="beam")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's B")
+    ap.add_argument("--logsumexp", action="store_true", help="log-sum-exp recombination variant")
+    ap.add_argument("--boost-rollback", action="store_true",
+                    help="end-of-utterance rollback of pending boosting")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-utts", type=int, default=8)
     ap.add_argument("--cpu-threads", type=int, default=8)
@@ -165,15 +168,16 @@ def main():
         nb_sc = torch.empty((B, K), dtype=torch.float32, device=dev)
 
     def launch(st=None):
+        fl = dict(logsumexp=args.logsumexp, boost_rollback=args.boost_rollback)
         if mode == "beam":
             P.ctcbeam_decode_ex(d_lp, d_len, K, w.alpha, w.beta, w.boost_w, lm, bt, ws, out_tok,
-                                out_len, out_sc, theta=w.theta, stats=st)
+                                out_len, out_sc, theta=w.theta, stats=st, **fl)
         elif mode == "nbest":
             P.ctcbeam_decode_nbest(d_lp, d_len, K, w.alpha, w.beta, w.boost_w, lm, bt, ws, nb_tok,
-                                   nb_len, nb_sc, theta=w.theta, stats=st)
+                                   nb_len, nb_sc, theta=w.theta, stats=st, **fl)
         else:
             P.ctcbeam_greedy_decode(d_lp, d_len, w.alpha, w.beta, w.boost_w, lm, bt, ws, out_tok,
-                                    out_len, out_sc, stats=st)
+                                    out_len, out_sc, stats=st, boost_rollback=args.boost_rollback)
 
     # untimed launch with the kernel's counters on: algorithmic bytes
     launch(stats)
@@ -213,7 +217,9 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "mode": mode, "B": B, "T": T, "V": V, "K": 1 if mode == "greedy" else K,
+        "config": {"workload": w.name, "mode": mode,
+                   "variants": [f for f, on in (("logsumexp", args.logsumexp),
+                                                ("boost_rollback", args.boost_rollback)) if on], "B": B, "T": T, "V": V, "K": 1 if mode == "greedy" else K,
                    "lm": None if w.lm is None else f"{w.lm.order}-gram, {'/'.join(str(c) for c in w.lm.counts)} explicit n-grams",
                    "boost": None if w.boost is None else f"{w.boost.n_phrases} phrases",
                    "alpha": w.alpha, "beta": w.beta, "boost_w": w.boost_w, "theta": w.theta,

@@ -153,12 +153,26 @@ int ctcbeam_decode(const float* logprobs, const int32_t* lengths, int B, int T, 
                    int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
                    hipStream_t stream);
 
+/* Variant flags (ctcbeam_opts.flags) for points Sec. III-C leaves open. */
+#define CTCBEAM_FLAG_LOGSUMEXP 1       /* recombination merges duplicate hypotheses
+                                          by log-sum-exp (summed probability of
+                                          their alignments) instead of max: the
+                                          lower slot takes lse(own, other) for each
+                                          later duplicate in slot order, with a
+                                          fixed fp32 exp / log1p (Cody-Waite
+                                          reduction + degree-7 Taylor polynomial;
+                                          atanh series) */
+#define CTCBEAM_FLAG_BOOST_ROLLBACK 2  /* after LM.Final, live hypotheses get
+                                          fl(boost_w * -pending), taking back the
+                                          boosting of an unfinished phrase */
+
 typedef struct ctcbeam_opts {
   float prune_theta;   /* Algorithm 1 threshold theta; +inf disables pruning */
   int64_t* stats;      /* device int64 [B, 8] or NULL: per-utterance counts of
                           frames, live beam-frames, LM chain states, LM arcs,
                           boosting chain nodes, boosting arcs, emitting winners */
-  int reserved[4];
+  int flags;           /* CTCBEAM_FLAG_* bits; unknown bits return 1 */
+  int reserved[3];
 } ctcbeam_opts;
 
 /* ctcbeam_decode with options (opts may be NULL: theta = +inf, no stats). */
@@ -201,7 +215,8 @@ int ctcbeam_decode_nbest(const float* logprobs, const int32_t* lengths, int B, i
  *   workspace    : device buffer of at least ctcbeam_workspace_bytes(B, 0, 1)
  *                  bytes (only the per-utterance status words are used; a
  *                  workspace sized for a beam decode of the same B fits)
- *   opts         : may be NULL; prune_theta is ignored; stats, when given,
+ *   opts         : may be NULL; prune_theta and CTCBEAM_FLAG_LOGSUMEXP are
+ *                  ignored (no effect with one hypothesis); stats, when given,
  *                  receives per utterance {frames, live frames, LM chain
  *                  states read, LM arcs read, boosting chain nodes, boosting
  *                  arcs, emitted tokens, state refills}

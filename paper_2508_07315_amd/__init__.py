@@ -97,7 +97,24 @@ def _check(rc: int):
 
 class _Opts(ctypes.Structure):
     _fields_ = [("prune_theta", ctypes.c_float), ("stats", ctypes.c_void_p),
-                ("reserved", ctypes.c_int * 4)]
+                ("flags", ctypes.c_int), ("reserved", ctypes.c_int * 3)]
+
+
+FLAG_LOGSUMEXP = 1        # CTCBEAM_FLAG_LOGSUMEXP
+FLAG_BOOST_ROLLBACK = 2   # CTCBEAM_FLAG_BOOST_ROLLBACK
+
+
+def _opts(theta, stats, B, logsumexp, boost_rollback):
+    """ctcbeam_opts by reference, or None when every option is at its default."""
+    import torch
+    flags = (FLAG_LOGSUMEXP if logsumexp else 0) | (FLAG_BOOST_ROLLBACK if boost_rollback else 0)
+    if (theta is None or math.isinf(theta)) and stats is None and flags == 0:
+        return None
+    o = _Opts()
+    o.prune_theta = float(theta if theta is not None else math.inf)
+    o.stats = None if stats is None else _dptr(stats, torch.int64, "stats", (B, 8)).value
+    o.flags = flags
+    return o
 
 
 class _LmView(ctypes.Structure):
@@ -274,7 +291,8 @@ def ctcbeam_decode_ex(logprobs, lengths, K: int, alpha: float = 0.0, beta: float
                       boost_w: float = 0.0, lm: Optional[LM] = None,
                       boost: Optional[Boost] = None, workspace=None, out_tokens=None,
                       out_lengths=None, out_scores=None, stream=None,
-                      theta: float = math.inf, stats=None):
+                      theta: float = math.inf, stats=None, logsumexp: bool = False,
+                      boost_rollback: bool = False):
     """Enqueue one decode on ``stream`` (default: torch's current stream).
 
     logprobs: float32 [B, T, V+1] device tensor (blank = V); lengths: int32 [B].
@@ -297,12 +315,8 @@ def ctcbeam_decode_ex(logprobs, lengths, K: int, alpha: float = 0.0, beta: float
     if workspace is None:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
     ws = _dptr(workspace, torch.uint8, "workspace")
-    opts = None
-    if (theta is not None and not math.isinf(theta)) or stats is not None:
-        o = _Opts()
-        o.prune_theta = float(theta if theta is not None else math.inf)
-        o.stats = None if stats is None else _dptr(stats, torch.int64, "stats", (B, 8)).value
-        opts = ctypes.byref(o)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback)
+    opts = None if o is None else ctypes.byref(o)
     if stream is None:
         stream = torch.cuda.current_stream(dev).cuda_stream
     rc = lib.ctcbeam_decode_ex(
@@ -329,7 +343,8 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
                          boost_w: float = 0.0, lm: Optional[LM] = None,
                          boost: Optional[Boost] = None, workspace=None, nbest_tokens=None,
                          nbest_lengths=None, nbest_scores=None, stream=None,
-                         theta: float = math.inf, stats=None):
+                         theta: float = math.inf, stats=None, logsumexp: bool = False,
+                         boost_rollback: bool = False):
     """Enqueue one N-best decode on ``stream`` (default: torch's current stream).
 
     Same inputs as ``ctcbeam_decode_ex``.  Returns (tokens [B,K,T] int32 with
@@ -353,12 +368,8 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
     if workspace is None:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
     ws = _dptr(workspace, torch.uint8, "workspace")
-    opts = None
-    if (theta is not None and not math.isinf(theta)) or stats is not None:
-        o = _Opts()
-        o.prune_theta = float(theta if theta is not None else math.inf)
-        o.stats = None if stats is None else _dptr(stats, torch.int64, "stats", (B, 8)).value
-        opts = ctypes.byref(o)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback)
+    opts = None if o is None else ctypes.byref(o)
     if stream is None:
         stream = torch.cuda.current_stream(dev).cuda_stream
     rc = lib.ctcbeam_decode_nbest(
@@ -375,7 +386,8 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
 def ctcbeam_greedy_decode(logprobs, lengths, alpha: float = 0.0, beta: float = 0.0,
                           boost_w: float = 0.0, lm: Optional[LM] = None,
                           boost: Optional[Boost] = None, workspace=None, out_tokens=None,
-                          out_lengths=None, out_scores=None, stream=None, stats=None):
+                          out_lengths=None, out_scores=None, stream=None, stats=None,
+                          boost_rollback: bool = False):
     """Enqueue one greedy decode with fusion (Algorithm 1 with one hypothesis)
     on ``stream``.  Returns (tokens [B,T] int32 with -1 padding, lengths [B],
     scores [B], workspace uint8)."""
@@ -396,12 +408,8 @@ def ctcbeam_greedy_decode(logprobs, lengths, alpha: float = 0.0, beta: float = 0
     if workspace is None:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
     ws = _dptr(workspace, torch.uint8, "workspace")
-    opts = None
-    if stats is not None:
-        o = _Opts()
-        o.prune_theta = math.inf
-        o.stats = _dptr(stats, torch.int64, "stats", (B, 8)).value
-        opts = ctypes.byref(o)
+    o = _opts(math.inf, stats, B, False, boost_rollback)
+    opts = None if o is None else ctypes.byref(o)
     if stream is None:
         stream = torch.cuda.current_stream(dev).cuda_stream
     rc = lib.ctcbeam_greedy_decode(

@@ -238,6 +238,54 @@ __device__ __forceinline__ float bitonic_levels(float v, int lane) {
   if constexpr (k < N) v = bitonic_levels<N, k * 2>(v, lane);
   return v;
 }
+// ---- fp32 log-sum-exp of the log-sum-exp recombination variant ----
+// Every step is one IEEE fp32 operation in a fixed order (no contraction), so
+// the result is reproducible bit for bit.  exp(d), -80 <= d <= 0: Cody-Waite
+// reduction d = k ln2 + r with k = rint(d / ln2) and ln2 split into a 9-bit
+// head (k * head is exact) and a tail, the degree-7 Taylor polynomial of e^r
+// by Horner, times 2^k built from its exponent bits.
+__device__ __forceinline__ float exp32_nonpos(float d) {
+  const float k = __builtin_rintf(d * 1.44269504f);
+  const float r = (d - k * 0.693359375f) - k * -2.12194440e-4f;
+  float q = 1.0f / 5040.0f;
+  q = q * r + 1.0f / 720.0f;
+  q = q * r + 1.0f / 120.0f;
+  q = q * r + 1.0f / 24.0f;
+  q = q * r + 1.0f / 6.0f;
+  q = q * r + 0.5f;
+  q = q * r + 1.0f;
+  q = q * r + 1.0f;
+  return q * __uint_as_float(static_cast<uint32_t>(static_cast<int>(k) + 127) << 23);
+}
+// log(1 + e), 2^-24 <= e <= 1: 2 atanh(s) with s = e / (2 + e) <= 1/3, the odd
+// series to s^17 by Horner in s^2.
+__device__ __forceinline__ float log1p32_unit(float e) {
+  const float s = e / (2.0f + e);
+  const float z = s * s;
+  float q = 1.0f / 17.0f;
+  q = q * z + 1.0f / 15.0f;
+  q = q * z + 1.0f / 13.0f;
+  q = q * z + 1.0f / 11.0f;
+  q = q * z + 1.0f / 9.0f;
+  q = q * z + 1.0f / 7.0f;
+  q = q * z + 1.0f / 5.0f;
+  q = q * z + 1.0f / 3.0f;
+  q = q * z + 1.0f;
+  const float t = s * q;
+  return t + t;
+}
+// log(exp(a) + exp(b))
+__device__ __forceinline__ float lse32(float a, float b) {
+  const float hi = (a < b) ? b : a;
+  const float lo = (a < b) ? a : b;
+  if (lo == kNegInf) return hi;
+  const float d = lo - hi;
+  if (d < -80.0f) return hi;
+  const float e = exp32_nonpos(d);
+  const float l = (e < 5.9604645e-8f) ? e : log1p32_unit(e);
+  return hi + l;
+}
+
 // Recombination probes at distances D = 1..DMAX: lane j against lane j-D of
 // its 16-lane row.  Lanes shifted in from outside the row read all ones.
 template <int D, int DMAX>
@@ -1019,6 +1067,23 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           dup = dup || (j > i && alive0 && rec[kRHlo] == hlo && rec[kRHhi] == hhi && meta == mi);
         }
       }
+      if (p.flags & kFlagLogSumExp) {  // uniform
+        // Each duplicate, in slot order, is merged into the first live slot
+        // of its transcript (a lower slot, which is not a duplicate itself).
+        uint64_t dm = __ballot(dup);
+        const float xs = x;
+        while (dm) {
+          const int jj = static_cast<int>(__builtin_ctzll(dm));
+          dm &= dm - 1ull;
+          const uint32_t hlo = rdlane(rec[kRHlo], jj);
+          const uint32_t hhi = rdlane(rec[kRHhi], jj);
+          const uint32_t mj = rdlane(meta, jj);
+          const uint64_t same = __ballot(alive0 && rec[kRHlo] == hlo && rec[kRHhi] == hhi && meta == mj);
+          const int rep = static_cast<int>(__builtin_ctzll(same));  // jj itself matches: same != 0
+          const float xj = rdlane(xs, jj);
+          if (j == rep && rep != jj) x = lse32(x, xj);
+        }
+      }
       if (dup) x = kNegInf;
       const bool nalive = alive0 && !dup;
       if (wave == 0 && j < K) bpb[static_cast<size_t>(t) * K + j] = valid ? static_cast<int32_t>(rec[kRBp]) : -1;
@@ -1133,6 +1198,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       }
       const float av = alpha * v;
       s = s + av;
+    }
+    if (HAS_BT && (p.flags & kFlagBoostRollback) && j < K && s != kNegInf) {
+      // the pending boosting of an unfinished phrase is taken back
+      const float wb = boost_w * static_cast<float>(-btpot);
+      s = s + wb;
     }
     // rank of each slot: final score descending, lowest slot on ties
     const float sj = (j < K) ? s : kNegInf;

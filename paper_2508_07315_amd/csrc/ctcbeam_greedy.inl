@@ -383,6 +383,11 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
     }
     s = s + alpha * v;
   }
+  if (!dead && HAS_BT && (p.flags & kFlagBoostRollback)) {
+    // the pending boosting of an unfinished phrase is taken back
+    const float wb = boost_w * static_cast<float>(-pot);
+    s = s + wb;
+  }
   if (dead) {
     s = kNegInf;
     nout = 0;

@@ -612,6 +612,9 @@ size_t ctcbeam_workspace_bytes(int B, int T, int K) {
   return status_bytes(B) + static_cast<size_t>(B) * static_cast<size_t>(T) * static_cast<size_t>(K) * sizeof(int32_t);
 }
 
+static_assert(CTCBEAM_FLAG_LOGSUMEXP == ctcbeam::kFlagLogSumExp, "flag values");
+static_assert(CTCBEAM_FLAG_BOOST_ROLLBACK == ctcbeam::kFlagBoostRollback, "flag values");
+
 namespace {
 
 // Shared body of the decode entry points: validation, parameter block and
@@ -635,6 +638,8 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
   const float theta = (opts && !greedy) ? opts->prune_theta : std::numeric_limits<float>::infinity();
   if (std::isnan(theta) || theta < 0.0f) return fail(1, "prune_theta must be >= 0 (or +inf)");
   if (std::isnan(alpha) || std::isnan(beta) || std::isnan(boost_w)) return fail(1, "NaN weight");
+  const int flags = opts ? opts->flags : 0;
+  if (flags & ~(CTCBEAM_FLAG_LOGSUMEXP | CTCBEAM_FLAG_BOOST_ROLLBACK)) return fail(1, "unknown flag bits");
   if (B == 0) return 0;
   if (!lengths || !workspace || (T > 0 && !logprobs)) return fail(1, "null device pointer");
   if (want_nbest ? (!nbest_lengths || !nbest_scores || (T > 0 && !nbest_tokens))
@@ -656,6 +661,7 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
   p.beta = beta;
   p.boost_w = boost_w;
   p.theta = theta;
+  p.flags = greedy ? (flags & ~CTCBEAM_FLAG_LOGSUMEXP) : flags;
   if (lm) {
     p.lm_states = lm->d_states;
     p.lm_arcs = lm->d_arcs;

@@ -14,6 +14,8 @@ constexpr int kKeyWords = 8192;       // per-chunk [hyp][token] key row entries
 constexpr int kLmStage = 4096;        // staged LM arcs per chunk (12-bit slot)
 constexpr int kCap = 512;             // survivor pool entries
 constexpr uint32_t kExists = 0x80000000u;
+constexpr int kFlagLogSumExp = 1;      // recombination by log-sum-exp
+constexpr int kFlagBoostRollback = 2;  // pending boosting taken back at the end
 
 // LM state record, one per chain level l (context of length l+1):
 //   {arc_begin, arc_count | kExists, backoff bits}
@@ -46,6 +48,7 @@ struct KernelParams {
   const int32_t* lengths;
   int B, T, V, K;
   float alpha, beta, boost_w, theta;
+  int flags;                 // kFlagLogSumExp | kFlagBoostRollback
   // LM (null when disabled)
   const LmLevel* lm_states;
   const LmArc* lm_arcs;
