@@ -114,9 +114,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=3, help="workload 1..5 (default 3)")
+    ap.add_argument("--config", type=int, default=3, help="workload 1..6 (default 3)")
     ap.add_argument("--mode", choices=("beam", "nbest", "greedy"), default="beam")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's B")
+    ap.add_argument("--beam", type=int, default=0, help="override the workload's K")
     ap.add_argument("--logsumexp", action="store_true", help="log-sum-exp recombination variant")
     ap.add_argument("--boost-rollback", action="store_true",
                     help="end-of-utterance rollback of pending boosting")
@@ -143,6 +144,8 @@ def main():
     w = W.CONFIGS[args.config]
     if args.batch > 0 and args.batch != w.B:
         w = w.replace(B=args.batch, name=re.sub(r"_B\d+_", f"_B{args.batch}_", w.name))
+    if args.beam > 0 and args.beam != w.K:
+        w = w.replace(K=args.beam, name=re.sub(r"_K\d+", f"_K{args.beam}", w.name))
     t_setup = time.perf_counter()
     lens = W.make_lengths(w)
     lp = W.make_logprobs(w)

@@ -47,6 +47,10 @@ def _load():
         raise ImportError(
             f"{LIB_PATH} is not built; run `python -m paper_2508_07315_amd.build_lib` "
             "(the decoder has no CPU fallback)")
+    # torch first: its HIP runtime and the system one share a SONAME, so the
+    # first loaded serves the whole process; it must be the one that owns
+    # torch's device memory and streams
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     P = ctypes.c_void_p
     I = ctypes.c_int

@@ -81,6 +81,8 @@ class Workload:
 
 LM3 = LMSpec(order=3, counts=(300_000, 1_000_000), seed=2003)
 LM4 = LMSpec(order=4, counts=(500_000, 3_000_000, 6_000_000), seed=2004)
+# paper-scale subword 6-gram (Sec. IV-A uses KenLM 6-grams): 11.0 M n-grams
+LM6 = LMSpec(order=6, counts=(500_000, 2_000_000, 3_000_000, 3_000_000, 2_500_000), seed=2006)
 
 CONFIGS = {
     1: Workload("cfg1_B2_T50_V32_K4", B=2, T=50, V=32, K=4, logits="gauss3",
@@ -97,6 +99,12 @@ CONFIGS = {
                 logits="peaky", lengths=("uniform", 100, 400), seed=1005,
                 alpha=0.5, beta=1.0, boost_w=1.5, lm=LM3,
                 boost=BoostSpec(5000, 2, 8, "zipf", 3005)),
+    # paper scale (Sec. V-C, Fig. "beam_size_vs_wer": batch 32, LM + PB,
+    # beams 4..128; Sec. IV-D: theta = 12): a 6-gram with 11 M n-grams
+    6: Workload("cfg6_B32_T400_V1024_K16_lm6_pb1000", B=32, T=400, V=1024, K=16,
+                logits="peaky", lengths=("uniform", 200, 400), seed=1006,
+                alpha=0.5, beta=1.0, boost_w=1.0, theta=12.0, lm=LM6,
+                boost=BoostSpec(1000, 2, 6, "uniform", 3006)),
 }
 
 
