@@ -416,13 +416,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     }
   }
   // beam record of live position lp (written by wave 0 for the live slots)
-  auto put_row = [&](int lp) {
+  auto put_row = [&](int lp) __attribute__((always_inline)) {
     uint32_t* rr = s_row + lp * kRowWords;
     *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc), static_cast<uint32_t>(last),
                                                static_cast<uint32_t>(j), static_cast<uint32_t>(btpot));
 #pragma unroll
     for (int l0 = 0; l0 < NL; l0 += 4) {
-      const auto bo_at = [&](int l) { return l < NL ? __float_as_uint(lvbo[l < NLA ? l : 0]) : 0u; };
+      const auto bo_at = [&](int l) __attribute__((always_inline)) { return l < NL ? __float_as_uint(lvbo[l < NLA ? l : 0]) : 0u; };
       *reinterpret_cast<uint4*>(rr + 4 + l0) = make_uint4(bo_at(l0), bo_at(l0 + 1), bo_at(l0 + 2), bo_at(l0 + 3));
     }
   };
@@ -460,7 +460,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     LmLevel hh[NLA];
     BtNode nd;
   };
-  auto succ_begin = [&](bool act, uint32_t idx, uint32_t lmt, uint32_t btk, const uint32_t* prec, Succ& sp) {
+  auto succ_begin = [&](bool act, uint32_t idx, uint32_t lmt, uint32_t btk, const uint32_t* prec, Succ& sp) __attribute__((always_inline)) {
     sp.par = act ? idx / static_cast<uint32_t>(W) : 0u;
     sp.c = act ? static_cast<int>(idx - sp.par * static_cast<uint32_t>(W)) : V;
     sp.lmt = lmt;
@@ -473,7 +473,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     sp.nd = BtNode{0u, 0u, 0u, 0u};
     if (HAS_BT) sp.nd = p.bt_nodes[sp.emit ? (btk & kBtChildMask) : 0u];
   };
-  auto succ_end = [&](Succ& sp, uint32_t xbits) {
+  auto succ_end = [&](Succ& sp, uint32_t xbits) __attribute__((always_inline)) {
     uint32_t* r = sp.r;
     const bool e = sp.emit;
     uint64_t h = (static_cast<uint64_t>(r[kRHhi]) << 32) | r[kRHlo];
@@ -736,7 +736,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         }
       }
       float cand[NC];
-      uint32_t lhi[NC], bkr[NC];
+      // without boosting the LM entries of the candidates fit in registers;
+      // with it they are re-read from the rows for the survivors
+      constexpr bool kKeepLm = HAS_LM && !HAS_BT;
+      uint32_t lhi[kKeepLm ? NC : 1];
       float lmax = kNegInf;
 #pragma unroll
       for (int i = 0; i < KCR; ++i) {
@@ -747,8 +750,6 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const uint32_t e = static_cast<uint32_t>(i * V) + rcc[jj];
           const float x0 = ksc[i] + rD[jj];
           float x1 = x0 + beta;
-          lhi[r] = 0u;
-          bkr[r] = 0u;
           if (HAS_LM) {
             const uint64_t ent = lmrow[e];
             const uint32_t hi = static_cast<uint32_t>(ent >> 32);
@@ -758,7 +759,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             const bool has = hi >= genhi;
             const float av = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
             x1 = x1 + av;
-            lhi[r] = has ? hi : 0u;
+            if constexpr (kKeepLm) lhi[r] = has ? hi : rcc[jj];
           }
           if (HAS_BT) {
             const uint32_t be = btrow[e];
@@ -766,13 +767,28 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             const int pre = static_cast<int>((bk >> 20) & 63u);
             const float bv = boost_w * static_cast<float>(pre - kpot[i]);
             x1 = x1 + bv;
-            bkr[r] = bk;
           }
           const float x = (c != klast[i]) ? x1 : x0;
           cand[r] = x;
           lmax = fmaxf(lmax, x);
         }
       }
+      // LM entry (staged, or the token's unigram state) and boosting key of
+      // candidate (i, jj), re-read from the rows for the few that are kept
+      // rather than held in registers from the scoring
+      auto cand_meta = [&](int i, int jj, uint32_t& lraw, uint32_t& bk) __attribute__((always_inline)) {
+        const uint32_t e = static_cast<uint32_t>(i * V) + rcc[jj];
+        lraw = 0u;
+        bk = 0u;
+        if (HAS_LM) {
+          const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
+          lraw = hi >= genhi ? hi : rcc[jj];
+        }
+        if (HAS_BT) {
+          const uint32_t be = btrow[e];
+          bk = (be >= genhi) ? be : rRoot[jj];
+        }
+      };
       if (ch == 0 && blank_lane) {
         // blank candidates of every slot into the reserved region
         const float x = sc + rBlank;
@@ -844,9 +860,14 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                 const int c = tid + jj * kThreads;
                 // LM target: staged entry (resolved by the rank) or the
                 // token's unigram state
-                const uint32_t lraw = HAS_LM ? (lhi[r] != 0u ? lhi[r] : static_cast<uint32_t>(c)) : 0u;
-                s_pool[slot] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lraw,
-                                          bkr[r]);
+                uint32_t lraw, bk;
+                if constexpr (kKeepLm) {
+                  lraw = lhi[r];
+                  bk = 0u;
+                } else {
+                  cand_meta(i, jj, lraw, bk);
+                }
+                s_pool[slot] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lraw, bk);
               } else {
                 s_overflow = 1;
               }
@@ -950,16 +971,25 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           int nk = 0;
           for (int it = 0; it < K; ++it) {
             uint64_t best = 0ull;
-            int who = -1;  // -1 none, 0..NC-1 register, 100+e reserved entry
+            int who = -1;  // -1 none, 0 a register candidate, 100+e reserved entry
+            // the best register candidate's fields, tracked by selects so that
+            // no candidate array is indexed at run time
+            float wx = kNegInf;
+            uint32_t wflat = 0u, wi = 0u, wjj = 0u;
 #pragma unroll
             for (int r = 0; r < NC; ++r) {
               if (cand[r] != kNegInf) {
                 const int i = r / LPT, jj = r % LPT;
                 const int c = tid + jj * kThreads;
-                const uint64_t key = order_key(cand[r], static_cast<uint32_t>(kslot[i] * W + c));
+                const uint32_t flat = static_cast<uint32_t>(kslot[i] * W + c);
+                const uint64_t key = order_key(cand[r], flat);
                 if (key < prev && key > best) {
                   best = key;
-                  who = r;
+                  who = 0;
+                  wx = cand[r];
+                  wflat = flat;
+                  wi = static_cast<uint32_t>(i);
+                  wjj = static_cast<uint32_t>(jj);
                 }
               }
             }
@@ -987,13 +1017,19 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             if (gbest == 0ull) break;  // nothing finite left (uniform)
             if (who >= 0 && best == gbest) {
               if (who < 100) {
-                const int r = who;
-                const int i = r / LPT, jj = r % LPT;
-                const int c = tid + jj * kThreads;
-                uint32_t lmt = 0u;
-                if (HAS_LM) lmt = lhi[r] != 0u ? tgt[lhi[r] & 0xFFFu] : static_cast<uint32_t>(c);
-                s_res[Q][it] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lmt,
-                                          bkr[r]);
+                // label c = tid + wjj * kThreads of chunk row wi
+                const uint32_t c = static_cast<uint32_t>(tid) + wjj * static_cast<uint32_t>(kThreads);
+                const uint32_t e = wi * static_cast<uint32_t>(V) + c;
+                uint32_t lmt = 0u, bk = 0u;
+                if (HAS_LM) {
+                  const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
+                  lmt = hi >= genhi ? tgt[hi & 0xFFFu] : c;
+                }
+                if (HAS_BT) {
+                  const uint32_t be = btrow[e];
+                  bk = (be >= genhi) ? be : p.bt_root_key[c];
+                }
+                s_res[Q][it] = make_uint4(__float_as_uint(wx), wflat, lmt, bk);
               } else {
                 s_res[Q][it] = s_res[P][who - 100];
               }

@@ -133,7 +133,7 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
   int32_t* ot = p.out_tokens + static_cast<size_t>(b) * T;
 
   // Rebuild the per-label terms for LM state `lms` and boosting node `btn`.
-  auto refill = [&](uint32_t lms, uint32_t btn) {
+  auto refill = [&](uint32_t lms, uint32_t btn) __attribute__((always_inline)) {
     BtNode nd{0u, 0u, 0u, 0u};
     if (HAS_LM) {
 #pragma unroll
@@ -196,13 +196,22 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
         a[u] = LmArc{0.0f, 0u, 0xFFFFFFFFu};
         e[u] = BtEntry{0xFFFFFFFFu, 0u};
         if (HAS_LM && tt < nt) {  // uniform
-          int lv = 0;
+          // the tile's level by a select chain (constant indices keep the
+          // chain headers in registers)
+          int lv = 0, t0l = tl[0];
+          uint32_t lb = hl[0].begin, lc = hl[0].count & ~kExists;
 #pragma unroll
-          for (int l = 1; l < NL; ++l) lv = (tt >= tl[l]) ? l : lv;
+          for (int l = 1; l < NL; ++l) {
+            const bool in = tt >= tl[l];
+            lv = in ? l : lv;
+            t0l = in ? tl[l] : t0l;
+            lb = in ? hl[l].begin : lb;
+            lc = in ? (hl[l].count & ~kExists) : lc;
+          }
           lvu[u] = lv;
-          const uint32_t q = static_cast<uint32_t>((tt - tl[lv]) * 64 + lane);
-          ok[u] = q < (hl[lv].count & ~kExists);
-          a[u] = p.lm_arcs[hl[lv].begin + (ok[u] ? q : 0u)];
+          const uint32_t q = static_cast<uint32_t>((tt - t0l) * 64 + lane);
+          ok[u] = q < lc;
+          a[u] = p.lm_arcs[lb + (ok[u] ? q : 0u)];
         } else if (HAS_BT && tt < nt + ntb) {  // uniform
           const uint32_t q = static_cast<uint32_t>((tt - nt) * 64 + lane);
           ok[u] = q < nd.list_count;
@@ -287,7 +296,7 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
     return emit;
   };
   // successor states of an emitted token (read before the refill overwrites)
-  auto next_states = [&](uint32_t& lms, uint32_t& btn) {
+  auto next_states = [&](uint32_t& lms, uint32_t& btn) __attribute__((always_inline)) {
     lms = HAS_LM ? static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(s_tg[last]))) : 0u;
     btn = HAS_BT ? static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(s_bk[last] & kBtChildMask)))
                  : 0u;
