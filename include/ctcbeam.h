@@ -55,7 +55,7 @@ typedef struct ctcbeam_lm ctcbeam_lm;
 typedef struct ctcbeam_boost ctcbeam_boost;
 
 /* Limits of this build (requests beyond them return 2). */
-#define CTCBEAM_MAX_K 64        /* beam size */
+#define CTCBEAM_MAX_K 128       /* beam size (above 64: V <= 1024) */
 #define CTCBEAM_MAX_V 4096      /* tokens (blank excluded) */
 #define CTCBEAM_MAX_ORDER 8     /* n-gram order */
 
@@ -135,7 +135,8 @@ size_t ctcbeam_workspace_bytes(int B, int T, int K);
  *                  of utterance b are read
  *   lengths      : device int32 [B]; values outside [0, T] are clamped and
  *                  flagged (ctcbeam_query_status)
- *   B, T, V, K   : batch, padded frames, tokens, beam size (1..CTCBEAM_MAX_K)
+ *   B, T, V, K   : batch, padded frames, tokens, beam size (1..CTCBEAM_MAX_K;
+ *                  beams above 64 need V <= 1024, else 2)
  *   alpha, beta, boost_w : weights of Eq. 1 (alpha ignored without an LM,
  *                  boost_w ignored without a boosting tree)
  *   lm, boost    : handles built on the current device, or NULL

@@ -24,7 +24,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libctcbeam.so")
 _lib = None
 
-MAX_K = 64
+MAX_K = 128           # CTCBEAM_MAX_K (beams above 64 need V <= 1024)
 MAX_V = 4096
 MAX_ORDER = 8
 

@@ -63,11 +63,6 @@ namespace detail {
 
 constexpr float kNegInf = -__builtin_huge_valf();
 
-// LDS scratch carved from one block so the traceback can reuse it:
-// [LM rows: kKeyWords x u64][boosting rows: kKeyWords x u32][LM targets].
-constexpr int kBigWords = 3 * kKeyWords + kLmStage;
-constexpr int kOffBtRow = 2 * kKeyWords;
-constexpr int kOffTgt = 3 * kKeyWords;
 // generation tag in the top 6 bits of LM entry high words and boosting keys
 constexpr int kGenShift = 26;
 constexpr uint32_t kGenMax = 63u;
@@ -304,13 +299,24 @@ __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
   return bitonic_levels<N, 2>(v, lane);
 }
 
-template <int LPT, int NLEV, bool HAS_BT>
+// SPL = beam slots per lane: slot j lives in lane j % 64, register set
+// j / 64 (SPL = 2 serves beams of 65..128).
+template <int LPT, int NLEV, bool HAS_BT, int SPL>
 __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool HAS_LM = NLEV >= 0;
   constexpr int NL = NLEV > 0 ? NLEV : 0;     // chain levels above the unigram root
   constexpr int NLA = NL > 0 ? NL : 1;        // array extent
   constexpr int NF = NL > 1 ? NL - 1 : 1;     // backoff weights folded into an arc (extent)
-  constexpr int KCR = 16 / LPT;               // beams (key rows) per chunk
+  constexpr int KMX = 64 * SPL;               // slot capacity
+  // beams (key rows) per chunk; two slots per lane leave LDS for 12 rows of
+  // 1024 labels instead of 16
+  constexpr int KCR = (SPL == 1 ? 16 : 12) / LPT;
+  // LDS scratch carved from one block so the traceback can reuse it:
+  // [LM rows: KW x u64][boosting rows: KW x u32][LM targets: kLmStage]
+  constexpr int KW = KCR * LPT * kThreads;
+  constexpr int kBigWords = 3 * KW + kLmStage;
+  constexpr int kOffBtRow = 2 * KW;
+  constexpr int kOffTgt = 3 * KW;
   constexpr int NC = KCR * LPT;               // candidates per lane
   // a chunk has at most 64 LM segments (beam, level): one lane each
   constexpr int KSEG = (NL > 0 && KCR * NL > 64) ? 64 / (NL > 0 ? NL : 1) : KCR;
@@ -327,12 +333,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // survivor pool: score bits, flat index, LM target (raw), boosting key
   __shared__ uint4 s_pool[kCap];
   // reserved regions (ping-pong): blank candidates, or the best K so far
-  __shared__ uint4 s_res[2][kMaxK];
+  __shared__ uint4 s_res[2][KMX];
   // beam records by live position: score, last label, slot, pot, backoff weights
-  __shared__ __align__(16) uint32_t s_row[(kMaxK + 16) * kRowWords];
+  __shared__ __align__(16) uint32_t s_row[(KMX + 16) * kRowWords];
   // beam state records by slot: [rcur] the current beam, [rcur ^ 1] its successors
-  __shared__ __align__(16) uint32_t s_rec[2 * kMaxK * RW];
-  __shared__ float s_top[kWaves * 8];
+  __shared__ __align__(16) uint32_t s_rec[2 * KMX * RW];
+  __shared__ float s_top[kWaves * 8 * SPL];
   __shared__ uint64_t s_red[2][kWaves];
   __shared__ int32_t s_nbuf, s_overflow;
   __shared__ int32_t s_best, s_bestlen;
@@ -378,56 +384,69 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     rDn[j] = ok ? (L > 0 ? Db[c] : 0.0f) : kNegInf;
     rD[j] = kNegInf;
   }
-  const bool blank_lane = (wave == 0) && (lane < K);
   float rBlankN = (L > 0 && lane < K) ? Db[V] : 0.0f;
   float rBlank = 0.0f;
 
-  // ---- beam state: slot j in lane j, replicated in every wave ----
+  // ---- beam state: slot j = lane + 64 h in register set h, replicated in
+  // every wave ----
   const int j = lane;
-  float sc = (j == 0) ? 0.0f : kNegInf;
-  int32_t last = V, len = 0;
-  uint32_t lvb[NLA], lvc[NLA];
-  float lvbo[NLA];
+  float sc[SPL];
+  int32_t last[SPL], len[SPL];
+  uint32_t lvb[SPL][NLA], lvc[SPL][NLA];
+  float lvbo[SPL][NLA];
+  uint32_t btb[SPL], btc[SPL];
+  int32_t btpot[SPL];
+  bool alive[SPL];
 #pragma unroll
-  for (int l = 0; l < NLA; ++l) {
-    lvb[l] = 0u;
-    lvc[l] = 0u;
-    lvbo[l] = 0.0f;
+  for (int h = 0; h < SPL; ++h) {
+    sc[h] = (h == 0 && j == 0) ? 0.0f : kNegInf;
+    last[h] = V;
+    len[h] = 0;
+#pragma unroll
+    for (int l = 0; l < NLA; ++l) {
+      lvb[h][l] = 0u;
+      lvc[h][l] = 0u;
+      lvbo[h][l] = 0.0f;
+    }
+    btb[h] = 0u;
+    btc[h] = 0u;
+    btpot[h] = 0;
+    alive[h] = h == 0 && j == 0;
   }
-  uint32_t btb = 0u, btc = 0u;
-  int32_t btpot = 0;
-  bool alive = (j == 0);
   const bool want_stats = p.stats != nullptr;
   if (j == 0) {
     if (HAS_LM) {
 #pragma unroll
       for (int l = 0; l < NL; ++l) {
-        const LmLevel h = p.lm_states[static_cast<size_t>(p.lm_bos_state) * NL + l];
-        lvb[l] = h.begin;
-        lvc[l] = h.count;
-        lvbo[l] = h.bo;
+        const LmLevel hd = p.lm_states[static_cast<size_t>(p.lm_bos_state) * NL + l];
+        lvb[0][l] = hd.begin;
+        lvc[0][l] = hd.count;
+        lvbo[0][l] = hd.bo;
       }
     }
     if (HAS_BT) {
       const BtNode nd = p.bt_nodes[0];
-      btb = nd.list_begin;
-      btc = nd.list_count;
-      btpot = static_cast<int32_t>(nd.pot & 0xFFu);
+      btb[0] = nd.list_begin;
+      btc[0] = nd.list_count;
+      btpot[0] = static_cast<int32_t>(nd.pot & 0xFFu);
     }
   }
-  // beam record of live position lp (written by wave 0 for the live slots)
-  auto put_row = [&](int lp) __attribute__((always_inline)) {
+  // beam record of live position lp for slot j + 64 h (written by wave 0 for
+  // the live slots)
+  auto put_row = [&](int lp, int h) __attribute__((always_inline)) {
     uint32_t* rr = s_row + lp * kRowWords;
-    *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc), static_cast<uint32_t>(last),
-                                               static_cast<uint32_t>(j), static_cast<uint32_t>(btpot));
+    *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc[h]), static_cast<uint32_t>(last[h]),
+                                               static_cast<uint32_t>(j + 64 * h), static_cast<uint32_t>(btpot[h]));
 #pragma unroll
     for (int l0 = 0; l0 < NL; l0 += 4) {
-      const auto bo_at = [&](int l) __attribute__((always_inline)) { return l < NL ? __float_as_uint(lvbo[l < NLA ? l : 0]) : 0u; };
+      const auto bo_at = [&](int l) __attribute__((always_inline)) { return l < NL ? __float_as_uint(lvbo[h][l < NLA ? l : 0]) : 0u; };
       *reinterpret_cast<uint4*>(rr + 4 + l0) = make_uint4(bo_at(l0), bo_at(l0 + 1), bo_at(l0 + 2), bo_at(l0 + 3));
     }
   };
   // chunk plan: chunk id of each live slot, number of chunks (uniform)
-  int cid = 0;
+  int cid[SPL];
+#pragma unroll
+  for (int h = 0; h < SPL; ++h) cid[h] = 0;
   int nch = 1;
   int rcur = 0;  // s_rec buffer holding the current beam
   // record helpers
@@ -502,24 +521,24 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   };
 
   for (int i = tid; i < kOffTgt; i += kThreads) s_big[i] = 0u;
-  for (int i = tid; i < (kMaxK + 16) * kRowWords; i += kThreads) s_row[i] = 0u;
+  for (int i = tid; i < (KMX + 16) * kRowWords; i += kThreads) s_row[i] = 0u;
   __syncthreads();
   if (tid == 0) {
-    put_row(0);
+    put_row(0, 0);
     // record of the initial beam (slot 0)
     uint32_t r[RW];
 #pragma unroll
     for (int w = 0; w < RW; ++w) r[w] = 0u;
     r[kRLast] = static_cast<uint32_t>(V);
     r[kRLms] = HAS_LM ? p.lm_bos_state : 0u;
-    r[kRBtb] = btb;
-    r[kRBtc] = btc;
-    r[kRBtp] = static_cast<uint32_t>(btpot);
+    r[kRBtb] = btb[0];
+    r[kRBtc] = btc[0];
+    r[kRBtp] = static_cast<uint32_t>(btpot[0]);
 #pragma unroll
     for (int l = 0; l < NL; ++l) {
-      r[kRLvb + l] = lvb[l];
-      r[kRLvc + l] = lvc[l];
-      r[kRLvbo + l] = __float_as_uint(lvbo[l]);
+      r[kRLvb + l] = lvb[0][l];
+      r[kRLvc + l] = lvc[0][l];
+      r[kRLvbo + l] = __float_as_uint(lvbo[0][l]);
     }
     store_rec(s_rec, r);
     s_nbuf = 0;
@@ -529,9 +548,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       unsigned long long ns = 0, na = 0;
 #pragma unroll
       for (int l = 0; l < NL; ++l) {
-        if (L > 0 && (lvc[l] & kExists)) {
+        if (L > 0 && (lvc[0][l] & kExists)) {
           ns += 1;
-          na += lvc[l] & ~kExists;
+          na += lvc[0][l] & ~kExists;
         }
       }
       s_st[0] = L > 0 ? 1 : 0;
@@ -565,10 +584,24 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     int cs = 0;  // live position of the chunk's first beam
 
     for (int ch = 0; ch < nch; ++ch) {
-      const bool inch = alive && (cid == ch);
-      const uint64_t chmask = __ballot(inch);
-      const int kc = __popcll(chmask);
-      const int row = __popcll(chmask & lmlt);
+      // this chunk's beams and their key rows (slot order)
+      bool inch[SPL];
+      int row[SPL];
+      int kc = 0;
+      if constexpr (SPL == 1) {
+        inch[0] = alive[0] && (cid[0] == ch);
+        const uint64_t chmask = __ballot(inch[0]);
+        kc = __popcll(chmask);
+        row[0] = __popcll(chmask & lmlt);
+      } else {
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          inch[h] = alive[h] && (cid[h] == ch);
+          const uint64_t chmask = __ballot(inch[h]);
+          row[h] = kc + __popcll(chmask & lmlt);
+          kc += __popcll(chmask);
+        }
+      }
 
       // ---- F. fill the key rows of this chunk ----
       if (gen == kGenMax) {
@@ -592,33 +625,37 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         for (int k = 0; k < NF; ++k) sg_f[k] = 0.0f;
 #pragma unroll
         for (int l = 0; l < NL; ++l) {
-          const uint32_t n = inch ? (lvc[l] & ~kExists) : 0u;
-          const uint64_t m = __ballot(n != 0u);
-          const int nl = __popcll(m);
-          if (nl > 0) {  // wave-uniform
-            // senders push to their segment lane; the rest to a lane outside
-            // [S, S + nl) (S + nl <= 64)
-            const int dst = (n != 0u) ? S + __popcll(m & lmlt) : ((S + nl) & 63);
-            const int addr = dst << 2;
-            const uint32_t r_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(n)));
-            const uint32_t r_base = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(lvb[l])));
-            const uint32_t r_rl =
-                static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, row | (l << 8)));
-            float r_f[NF];
 #pragma unroll
-            for (int k = 0; k + 1 < NL; ++k) {
-              const int lk = l + 1 + k;
-              const float fk = lk < NL ? lvbo[lk < NLA ? lk : 0] : 0.0f;
-              r_f[k] = __int_as_float(__builtin_amdgcn_ds_permute(addr, __float_as_int(fk)));
-            }
-            if (lane >= S && lane < S + nl) {
-              sg_cnt = r_cnt;
-              sg_base = r_base;
-              sg_rl = r_rl;
+          for (int h = 0; h < SPL; ++h) {
+            const uint32_t n = inch[h] ? (lvc[h][l] & ~kExists) : 0u;
+            const uint64_t m = __ballot(n != 0u);
+            const int nl = __popcll(m);
+            if (nl > 0) {  // wave-uniform
+              // senders push to their segment lane; the rest to a lane outside
+              // [S, S + nl) (S + nl <= 64)
+              const int dst = (n != 0u) ? S + __popcll(m & lmlt) : ((S + nl) & 63);
+              const int addr = dst << 2;
+              const uint32_t r_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(n)));
+              const uint32_t r_base =
+                  static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(lvb[h][l])));
+              const uint32_t r_rl =
+                  static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, row[h] | (l << 8)));
+              float r_f[NF];
 #pragma unroll
-              for (int k = 0; k + 1 < NL; ++k) sg_f[k] = r_f[k];
+              for (int k = 0; k + 1 < NL; ++k) {
+                const int lk = l + 1 + k;
+                const float fk = lk < NL ? lvbo[h][lk < NLA ? lk : 0] : 0.0f;
+                r_f[k] = __int_as_float(__builtin_amdgcn_ds_permute(addr, __float_as_int(fk)));
+              }
+              if (lane >= S && lane < S + nl) {
+                sg_cnt = r_cnt;
+                sg_base = r_base;
+                sg_rl = r_rl;
+#pragma unroll
+                for (int k = 0; k + 1 < NL; ++k) sg_f[k] = r_f[k];
+              }
+              S += nl;
             }
-            S += nl;
           }
         }
         // tiles of 64 arcs never straddle segments: a tile's segment is one
@@ -669,16 +706,28 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       }
       if (HAS_BT) {
         // same scheme, one segment per beam (its merged continuation list)
-        const uint32_t nb = inch ? btc : 0u;
-        const uint64_t m = __ballot(nb != 0u);
-        const int S = __popcll(m);
+        int S = 0;
+        uint32_t bg_cnt = 0u, bg_base = 0u, bg_row = 0u;
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          const uint32_t nb = inch[h] ? btc[h] : 0u;
+          const uint64_t m = __ballot(nb != 0u);
+          const int nl = __popcll(m);
+          if (nl > 0) {  // wave-uniform
+            const int dst = (nb != 0u) ? S + __popcll(m & lmlt) : ((S + nl) & 63);
+            const int addr = dst << 2;
+            const uint32_t r_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(nb)));
+            const uint32_t r_base = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(btb[h])));
+            const uint32_t r_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, row[h]));
+            if (lane >= S && lane < S + nl) {
+              bg_cnt = r_cnt;
+              bg_base = r_base;
+              bg_row = r_row;
+            }
+            S += nl;
+          }
+        }
         if (S > 0) {  // wave-uniform
-          const int dst = (nb != 0u) ? __popcll(m & lmlt) : (S & 63);
-          const int addr = dst << 2;
-          uint32_t bg_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(nb)));
-          const uint32_t bg_base = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(btb)));
-          const uint32_t bg_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(row)));
-          if (lane >= S) bg_cnt = 0u;
           const int btl = static_cast<int>((bg_cnt + 63u) >> 6);
           const int tincl = wave_incl_scan(btl, lane);
           const int texcl = tincl - btl;
@@ -789,12 +838,23 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           bk = (be >= genhi) ? be : rRoot[jj];
         }
       };
-      if (ch == 0 && blank_lane) {
+      if (SPL == 1 && ch == 0 && wave == 0 && lane < K) {
         // blank candidates of every slot into the reserved region
-        const float x = sc + rBlank;
-        const bool ok = sc != kNegInf && x != kNegInf;
+        const float x = sc[0] + rBlank;
+        const bool ok = sc[0] != kNegInf && x != kNegInf;
         s_res[mpar][j] = make_uint4(__float_as_uint(ok ? x : kNegInf),
                                     ok ? static_cast<uint32_t>(j * W + V) : 0xFFFFFFFFu, 0u, 0u);
+      } else if (SPL > 1 && ch == 0 && wave == 0) {
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          const int js = j + 64 * h;
+          if (js < K) {
+            const float x = sc[h] + rBlank;
+            const bool ok = sc[h] != kNegInf && x != kNegInf;
+            s_res[mpar][js] = make_uint4(__float_as_uint(ok ? x : kNegInf),
+                                         ok ? static_cast<uint32_t>(js * W + V) : 0xFFFFFFFFu, 0u, 0u);
+          }
+        }
       }
       if (tid == 0) {
         s_nbuf = 0;  // the previous rank read it before barrier D
@@ -803,8 +863,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       // Maxima of disjoint lane groups are distinct candidates, so the K-th
       // largest of at least K group maxima bounds the K-th best candidate
       // from below.  K <= 8: the 8 wave maxima; K <= 32: the 32 rows of 16
-      // lanes; otherwise 64 groups of 8 lanes.
-      if (K <= 8) {
+      // lanes; K <= 64: 64 groups of 8 lanes; otherwise 128 groups of 4.
+      if (SPL > 1) {
+        float g = fmax_sel(lmax, xor_lane(lmax, 1, lane));
+        g = fmax_sel(g, xor_lane(g, 2, lane));
+        if ((lane & 3) == 3) s_top[wave * 16 + (lane >> 2)] = g;
+      } else if (K <= 8) {
         const float g = row_max_last(lmax);
         const float g2 = fmax_sel(fmax_sel(rdlane(g, 15), rdlane(g, 31)), fmax_sel(rdlane(g, 47), rdlane(g, 63)));
         if (lane == 0) s_top[wave] = g2;
@@ -826,13 +890,40 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         } else if (K <= 32) {
           const float v = wave_sort_desc<32>(lane < 32 ? s_top[lane] : kNegInf, lane);
           tc = rdlane(v, K - 1);
-        } else {
+        } else if (SPL == 1) {
           const float v = wave_sort_desc<64>(s_top[lane], lane);
           tc = rdlane(v, K - 1);
+        } else {
+          // K-th largest of 128 maxima, two sorted halves a and b: the largest
+          // value x with at least K maxima >= x (counts by binary search)
+          const float a = wave_sort_desc<64>(s_top[lane], lane);
+          const float bb = wave_sort_desc<64>(s_top[64 + lane], lane);
+          const float a_last = rdlane(a, 63), b_last = rdlane(bb, 63);
+          auto count_ge = [&](float x) __attribute__((always_inline)) {
+            // #{a >= x}: 64 if the smallest is, else a search over counts 0..63
+            int pa = 0, pb = 0;
+#pragma unroll
+            for (int step = 32; step >= 1; step >>= 1) {
+              const float va = __int_as_float(__builtin_amdgcn_ds_bpermute((pa + step - 1) << 2, __float_as_int(a)));
+              const float vb = __int_as_float(__builtin_amdgcn_ds_bpermute((pb + step - 1) << 2, __float_as_int(bb)));
+              pa += (va >= x) ? step : 0;
+              pb += (vb >= x) ? step : 0;
+            }
+            return (a_last >= x ? 64 : pa) + (b_last >= x ? 64 : pb);
+          };
+          const float ca = count_ge(a) >= K ? a : kNegInf;
+          const float cb = count_ge(bb) >= K ? bb : kNegInf;
+          float v = fmax_sel(ca, cb);
+#pragma unroll
+          for (int d = 1; d < 64; d <<= 1) v = fmax_sel(v, xor_lane(v, d, lane));
+          tc = v;
         }
         // the blank candidates are exact: with K live slots the smallest
         // blank score also bounds the K-th best from below
-        float tb = (lane < K) ? sc + rBlank : __builtin_huge_valf();
+        float tb = (lane < K) ? sc[0] + rBlank : __builtin_huge_valf();
+#pragma unroll
+        for (int h = 1; h < SPL; ++h)
+          if (j + 64 * h < K) tb = fmin_sel(tb, sc[h] + rBlank);
         tb = fmin_sel(tb, xor_lane(tb, 1, lane));
         tb = fmin_sel(tb, xor_lane(tb, 2, lane));
         tb = fmin_sel(tb, xor_lane(tb, 4, lane));
@@ -884,8 +975,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       {
         const int P = mpar, Q = mpar ^ 1;
         const bool last_chunk = ch + 1 == nch;
-        const uint32_t* prec = s_rec + rcur * (kMaxK * RW);
-        uint32_t* nrec = s_rec + (rcur ^ 1) * (kMaxK * RW);
+        const uint32_t* prec = s_rec + rcur * (KMX * RW);
+        uint32_t* nrec = s_rec + (rcur ^ 1) * (KMX * RW);
         if (!s_overflow) {
           const int n = min(s_nbuf, kCap);
           const int N = K + n;
@@ -1040,18 +1131,19 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           nfin = nk;
           if (last_chunk) {
             __syncthreads();  // region Q complete
-            const bool act = wave == 0 && lane < nk;
+            // rank tid (waves 0 .. SPL-1)
+            const bool act = (SPL > 1 || wave == 0) && tid < nk;
             uint4 e = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
-            if (act) e = s_res[Q][lane];
+            if (act) e = s_res[Q][tid];
             Succ sp;
             succ_begin(act, e.y, e.z, e.w, prec, sp);
             succ_end(sp, e.x);
-            if (act) store_rec(nrec + lane * RW, sp.r);
+            if (act) store_rec(nrec + tid * RW, sp.r);
           }
         }
         // ranks [nfin, K) hold no candidate (the next chunk reads all K)
-        if (!last_chunk && wave == 0 && lane >= nfin && lane < K)
-          s_res[Q][lane] = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+        if (!last_chunk && (SPL > 1 || wave == 0) && tid >= nfin && tid < K)
+          s_res[Q][tid] = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
       }
       __syncthreads();  // D: best K of the chunk in region Q
       mpar ^= 1;
@@ -1059,6 +1151,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       cs += kc;
     }
 
+    // The single-slot form (K <= 64) is kept apart from the general one: the
+    // general form, instantiated with one slot per lane, changes the register
+    // allocation of the frame loop and costs about 2 % at K = 8.
+    if constexpr (SPL == 1) {
     // ---- U. prune, recombine, take the new beam (every wave, lane j = slot j) ----
     {
       const int nsel = min(K, nfin);
@@ -1066,7 +1162,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       uint32_t rec[RW];
 #pragma unroll
       for (int w = 0; w < RW; ++w) rec[w] = 0u;
-      if (valid) load_rec(s_rec + (rcur ^ 1) * (kMaxK * RW) + j * RW, rec);
+      if (valid) load_rec(s_rec + (rcur ^ 1) * (KMX * RW) + j * RW, rec);
       float x = valid ? __uint_as_float(rec[kRX]) : kNegInf;
       // prune (Algorithm 1: below best - theta -> -inf)
       const float best = rdlane(x, 0);
@@ -1124,22 +1220,22 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       const bool nalive = alive0 && !dup;
       if (wave == 0 && j < K) bpb[static_cast<size_t>(t) * K + j] = valid ? static_cast<int32_t>(rec[kRBp]) : -1;
       // new state
-      sc = x;
-      last = nlast;
-      len = nlen;
-      alive = nalive;
+      sc[0] = x;
+      last[0] = nlast;
+      len[0] = nlen;
+      alive[0] = nalive;
       int32_t acnt = 0;
 #pragma unroll
       for (int l = 0; l < NL; ++l) {
-        lvb[l] = nalive ? rec[kRLvb + l] : 0u;
-        lvc[l] = nalive ? rec[kRLvc + l] : 0u;
-        lvbo[l] = nalive ? __uint_as_float(rec[kRLvbo + l]) : 0.0f;
-        acnt += static_cast<int32_t>(lvc[l] & ~kExists);
+        lvb[0][l] = nalive ? rec[kRLvb + l] : 0u;
+        lvc[0][l] = nalive ? rec[kRLvc + l] : 0u;
+        lvbo[0][l] = nalive ? __uint_as_float(rec[kRLvbo + l]) : 0.0f;
+        acnt += static_cast<int32_t>(lvc[0][l] & ~kExists);
       }
       if (HAS_BT) {
-        btb = nalive ? rec[kRBtb] : 0u;
-        btc = nalive ? rec[kRBtc] : 0u;
-        btpot = nalive ? static_cast<int32_t>(rec[kRBtp]) : 0;
+        btb[0] = nalive ? rec[kRBtb] : 0u;
+        btc[0] = nalive ? rec[kRBtc] : 0u;
+        btpot[0] = nalive ? static_cast<int32_t>(rec[kRBtp]) : 0;
       }
       if (want_stats && wave == 0) {
         // chain work of the next frame (alive beams) and this frame's
@@ -1149,9 +1245,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         if (counted) {
 #pragma unroll
           for (int l = 0; l < NL; ++l) {
-            if (lvc[l] & kExists) {
+            if (lvc[0][l] & kExists) {
               s_ls += 1u;
-              s_la += lvc[l] & ~kExists;
+              s_la += lvc[0][l] & ~kExists;
             }
           }
           if (HAS_BT) {
@@ -1172,17 +1268,17 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       const uint64_t amask = __ballot(nalive);
       const int na = __popcll(amask);
       const int lp = __popcll(amask & lmlt);
-      if (wave == 0 && nalive) put_row(lp);
+      if (wave == 0 && nalive) put_row(lp, 0);
       // chunk plan: live slots in slot order, at most kcmax beams and
       // kLmStage staged arcs per chunk
       const int ia = wave_incl_scan(acnt, lane);
       const int tota = rdlane(ia, 63);
       if (na <= kcmax && tota <= kLmStage) {
         nch = na > 0 ? 1 : 0;
-        cid = 0;
+        cid[0] = 0;
       } else {
         nch = 0;
-        cid = -1;
+        cid[0] = -1;
         int start = 0;
         while (start < na) {
           const uint64_t sm = __ballot(nalive && lp == start);
@@ -1194,18 +1290,219 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             cnt = 1;  // a single chain above the staging limit (the builders prevent it)
             status |= 4u;
           }
-          if (nalive && lp >= start && lp < start + cnt) cid = nch;
+          if (nalive && lp >= start && lp < start + cnt) cid[0] = nch;
           ++nch;
           start += cnt;
         }
       }
     }
+    } else {
+    // ---- U. prune, recombine, take the new beam (every wave; slot
+    // j + 64 h in register set h) ----
+    {
+      const int nsel = min(K, nfin);
+      uint32_t rec[SPL][RW];
+      float x[SPL];
+      bool valid[SPL], alive0[SPL], dup[SPL], emit_fin[SPL];
+      int32_t nlast[SPL], nlen[SPL];
+      uint32_t meta[SPL];
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        valid[h] = j + 64 * h < nsel;
+#pragma unroll
+        for (int w = 0; w < RW; ++w) rec[h][w] = 0u;
+        if (valid[h]) load_rec(s_rec + (rcur ^ 1) * (KMX * RW) + (j + 64 * h) * RW, rec[h]);
+        x[h] = valid[h] ? __uint_as_float(rec[h][kRX]) : kNegInf;
+      }
+      // prune (Algorithm 1: below best - theta -> -inf)
+      const float best = rdlane(x[0], 0);
+      const float lim = best - p.theta;
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        if (valid[h] && x[h] < lim) x[h] = kNegInf;
+        const bool emit = valid[h] && rec[h][kREmit] != 0u;
+        emit_fin[h] = x[h] != kNegInf && emit;
+        nlast[h] = valid[h] ? static_cast<int32_t>(rec[h][kRLast]) : V;
+        nlen[h] = static_cast<int32_t>(rec[h][kRLen]);
+        // recombination key: transcript hash, length and ends-in-blank flag
+        alive0[h] = valid[h] && x[h] != kNegInf;
+        meta[h] = (static_cast<uint32_t>(nlen[h]) & 0x3FFFFFFFu) | ((nlast[h] == V ? 1u : 0u) << 30);
+        dup[h] = false;
+      }
+      if (K <= 16) {
+        // The K slots sit in the first 16-lane row: compare each with the
+        // slots below it through row shifts.  The key folds the length and
+        // the ends-in-blank flag into the 64-bit transcript hash (a false
+        // merge needs a 64-bit collision, as for the hash itself); dead
+        // slots use all ones and are never merged into.
+        uint64_t key = ((static_cast<uint64_t>(rec[0][kRHhi]) << 32) | rec[0][kRHlo]) ^
+                       (static_cast<uint64_t>(meta[0] + 1u) * 0xD6E8FEB86659FD93ull);
+        if (!alive0[0]) key = ~0ull;
+        const uint32_t klo = static_cast<uint32_t>(key), khi = static_cast<uint32_t>(key >> 32);
+        dup[0] = (K <= 8 ? recomb_shifts<1, 7>(klo, khi) : recomb_shifts<1, 15>(klo, khi)) && alive0[0];
+      } else {
+        // every live slot i against the slots above it, in slot order
+#pragma unroll
+        for (int hi = 0; hi < SPL; ++hi) {
+          uint64_t mr = __ballot(alive0[hi]);
+          if (hi == SPL - 1) mr &= ~(1ull << 63);  // the top slot is never the lower one
+          while (mr) {
+            const int i = static_cast<int>(__builtin_ctzll(mr));
+            mr &= mr - 1ull;
+            const uint32_t hlo = rdlane(rec[hi][kRHlo], i);
+            const uint32_t hhi = rdlane(rec[hi][kRHhi], i);
+            const uint32_t mi = rdlane(meta[hi], i);
+#pragma unroll
+            for (int h = 0; h < SPL; ++h)
+              dup[h] = dup[h] || (j + 64 * h > i + 64 * hi && alive0[h] && rec[h][kRHlo] == hlo &&
+                                  rec[h][kRHhi] == hhi && meta[h] == mi);
+          }
+        }
+      }
+      if (p.flags & kFlagLogSumExp) {  // uniform
+        // Each duplicate, in slot order, is merged into the first live slot
+        // of its transcript (a lower slot, which is not a duplicate itself).
+        float xs[SPL];
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) xs[h] = x[h];
+#pragma unroll
+        for (int hj = 0; hj < SPL; ++hj) {
+          uint64_t dm = __ballot(dup[hj]);
+          while (dm) {
+            const int jj = static_cast<int>(__builtin_ctzll(dm));
+            dm &= dm - 1ull;
+            const uint32_t hlo = rdlane(rec[hj][kRHlo], jj);
+            const uint32_t hhi = rdlane(rec[hj][kRHhi], jj);
+            const uint32_t mj = rdlane(meta[hj], jj);
+            int rep = -1;  // the duplicate itself matches, so some slot does
+#pragma unroll
+            for (int h = SPL - 1; h >= 0; --h) {
+              const uint64_t same =
+                  __ballot(alive0[h] && rec[h][kRHlo] == hlo && rec[h][kRHhi] == hhi && meta[h] == mj);
+              if (same) rep = static_cast<int>(__builtin_ctzll(same)) + 64 * h;
+            }
+            const float xj = rdlane(xs[hj], jj);
+#pragma unroll
+            for (int h = 0; h < SPL; ++h)
+              if (j + 64 * h == rep && rep != jj + 64 * hj) x[h] = lse32(x[h], xj);
+          }
+        }
+      }
+      bool nalive[SPL];
+      int32_t acnt[SPL];
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        if (dup[h]) x[h] = kNegInf;
+        nalive[h] = alive0[h] && !dup[h];
+        const int js = j + 64 * h;
+        if (wave == 0 && js < K)
+          bpb[static_cast<size_t>(t) * K + js] = valid[h] ? static_cast<int32_t>(rec[h][kRBp]) : -1;
+        // new state
+        sc[h] = x[h];
+        last[h] = nlast[h];
+        len[h] = nlen[h];
+        alive[h] = nalive[h];
+        acnt[h] = 0;
+#pragma unroll
+        for (int l = 0; l < NL; ++l) {
+          lvb[h][l] = nalive[h] ? rec[h][kRLvb + l] : 0u;
+          lvc[h][l] = nalive[h] ? rec[h][kRLvc + l] : 0u;
+          lvbo[h][l] = nalive[h] ? __uint_as_float(rec[h][kRLvbo + l]) : 0.0f;
+          acnt[h] += static_cast<int32_t>(lvc[h][l] & ~kExists);
+        }
+        if (HAS_BT) {
+          btb[h] = nalive[h] ? rec[h][kRBtb] : 0u;
+          btc[h] = nalive[h] ? rec[h][kRBtc] : 0u;
+          btpot[h] = nalive[h] ? static_cast<int32_t>(rec[h][kRBtp]) : 0;
+        }
+        if (want_stats && wave == 0) {
+          // chain work of the next frame (alive beams) and this frame's
+          // emitting winners
+          uint32_t s_ls = 0u, s_la = 0u, s_bn = 0u, s_ba = 0u;
+          const bool counted = t + 1 < L && nalive[h];
+          if (counted) {
+#pragma unroll
+            for (int l = 0; l < NL; ++l) {
+              if (lvc[h][l] & kExists) {
+                s_ls += 1u;
+                s_la += lvc[h][l] & ~kExists;
+              }
+            }
+            if (HAS_BT) {
+              const BtNode pn = p.bt_nodes[rec[h][kRBts]];
+              s_bn = pn.pot >> 8;
+              s_ba = pn.chain_arcs;
+            }
+            atomicAdd(&s_st[0], 1ull);
+          }
+          if (s_ls) atomicAdd(&s_st[1], static_cast<unsigned long long>(s_ls));
+          if (s_la) atomicAdd(&s_st[2], static_cast<unsigned long long>(s_la));
+          if (s_bn) atomicAdd(&s_st[3], static_cast<unsigned long long>(s_bn));
+          if (s_ba) atomicAdd(&s_st[4], static_cast<unsigned long long>(s_ba));
+          if (emit_fin[h]) atomicAdd(&s_st[5], 1ull);
+        }
+      }
+      rcur ^= 1;
+      // live positions (slot order) and beam records for the next frame;
+      // ia = inclusive scan of the staged arcs over the slots
+      int lp[SPL], ia[SPL];
+      int na = 0, tota = 0;
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        const uint64_t amask = __ballot(nalive[h]);
+        lp[h] = na + __popcll(amask & lmlt);
+        na += __popcll(amask);
+        if (wave == 0 && nalive[h]) put_row(lp[h], h);
+        ia[h] = tota + wave_incl_scan(acnt[h], lane);
+        tota = rdlane(ia[h], 63);
+      }
+      // chunk plan: live slots in slot order, at most kcmax beams and
+      // kLmStage staged arcs per chunk
+      if (na <= kcmax && tota <= kLmStage) {
+        nch = na > 0 ? 1 : 0;
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) cid[h] = 0;
+      } else {
+        nch = 0;
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) cid[h] = -1;
+        int start = 0;
+        while (start < na) {
+          // staged arcs before the chunk's first beam (the slot at live
+          // position start)
+          int basea = 0;
+#pragma unroll
+          for (int h = SPL - 1; h >= 0; --h) {
+            const uint64_t sm = __ballot(nalive[h] && lp[h] == start);
+            if (sm) basea = rdlane(ia[h] - acnt[h], static_cast<int>(__builtin_ctzll(sm)));
+          }
+          int cnt = 0;
+#pragma unroll
+          for (int h = 0; h < SPL; ++h) {
+            const bool ok = nalive[h] && lp[h] >= start && lp[h] < start + kcmax && (ia[h] - basea) <= kLmStage;
+            cnt += __popcll(__ballot(ok));
+          }
+          if (cnt == 0) {
+            cnt = 1;  // a single chain above the staging limit (the builders prevent it)
+            status |= 4u;
+          }
+#pragma unroll
+          for (int h = 0; h < SPL; ++h)
+            if (nalive[h] && lp[h] >= start && lp[h] < start + cnt) cid[h] = nch;
+          ++nch;
+          start += cnt;
+        }
+      }
+    }
+    }
   }
 
+  // single-slot and general forms kept apart, as for the beam update
+  if constexpr (SPL == 1) {
   // ---- LM.Final, order of the final hypotheses ----
   const bool nbest = p.nbest_scores != nullptr;
   if (wave == 0) {
-    float s = sc;
+    float s = sc[0];
     if (HAS_LM && j < K && s != kNegInf) {
       // ln P(</s> | state) through the backoff chain; </s> is the last arc of
       // a state's sorted arcs when present
@@ -1214,9 +1511,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       float fv = 0.0f;
 #pragma unroll
       for (int l = NL - 1; l >= 0; --l) {
-        const uint32_t n = lvc[l] & ~kExists;
+        const uint32_t n = lvc[0][l] & ~kExists;
         if (found < 0 && n > 0) {
-          const LmArc a = p.lm_arcs[lvb[l] + n - 1];
+          const LmArc a = p.lm_arcs[lvb[0][l] + n - 1];
           if (a.token == static_cast<uint32_t>(V)) {
             found = l;
             fv = a.logp;
@@ -1227,17 +1524,17 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         v = fv;
 #pragma unroll
         for (int l = 0; l < NL; ++l)
-          if (l > found) v = v + lvbo[l];
+          if (l > found) v = v + lvbo[0][l];
       } else {
 #pragma unroll
-        for (int l = 0; l < NL; ++l) v = v + lvbo[l];
+        for (int l = 0; l < NL; ++l) v = v + lvbo[0][l];
       }
       const float av = alpha * v;
       s = s + av;
     }
     if (HAS_BT && (p.flags & kFlagBoostRollback) && j < K && s != kNegInf) {
       // the pending boosting of an unfinished phrase is taken back
-      const float wb = boost_w * static_cast<float>(-btpot);
+      const float wb = boost_w * static_cast<float>(-btpot[0]);
       s = s + wb;
     }
     // rank of each slot: final score descending, lowest slot on ties
@@ -1250,13 +1547,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     const uint64_t top = __ballot(j < K && rank == 0);
     const int bj = static_cast<int>(__builtin_ctzll(top));  // K >= 1: some slot has rank 0
     const float bs = rdlane(sj, bj);
-    const int blen = rdlane(len, bj);
-    const int nlen = (j < K && sj != kNegInf) ? len : 0;
+    const int blen = rdlane(len[0], bj);
+    const int nlen = (j < K && sj != kNegInf) ? len[0] : 0;
     if (nbest && j < K) {
       p.nbest_scores[static_cast<size_t>(b) * K + rank] = sj;
       p.nbest_lengths[static_cast<size_t>(b) * K + rank] = nlen;
       s_row[rank] = static_cast<uint32_t>(nlen);  // lengths by rank (the row table is free now)
-      s_row[kMaxK + j] = static_cast<uint32_t>(rank);
+      s_row[KMX + j] = static_cast<uint32_t>(rank);
     }
     if (lane == 0) {
       s_best = bj;
@@ -1299,15 +1596,15 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // walks slot j (every live slot) and writes the row of its rank.
   // (the LM.Final term is finite, so some slot is live exactly when the best
   // final score is finite)
-  const bool walker = (wave == 0) && (nbest ? (j < K && sc != kNegInf) : (lane == 0 && have));
+  const bool walker = (wave == 0) && (nbest ? (j < K && sc[0] != kNegInf) : (lane == 0 && have));
   if (have && L > 0) {
     const int tile_frames = kBigWords / K;
     int jb = nbest ? j : best, cnext = -1;
     int32_t* orow = nullptr;
     int pos = 0;
     if (walker) {
-      orow = nbest ? nbt + static_cast<size_t>(s_row[kMaxK + j]) * T : ot;
-      pos = nbest ? len : nout;
+      orow = nbest ? nbt + static_cast<size_t>(s_row[KMX + j]) * T : ot;
+      pos = nbest ? len[0] : nout;
     }
     for (int hi = L; hi > 0;) {
       const int lo = hi > tile_frames ? hi - tile_frames : 0;
@@ -1341,33 +1638,218 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     }
     if (wave == 0 && __ballot(walker && pos != 0) != 0ull) status |= 2u;
   }
+  } else {
+  // ---- LM.Final, order of the final hypotheses ----
+  const bool nbest = p.nbest_scores != nullptr;
+  if (wave == 0) {
+    float sj[SPL];
+#pragma unroll
+    for (int h = 0; h < SPL; ++h) {
+      const int js = j + 64 * h;
+      float s = sc[h];
+      if (HAS_LM && js < K && s != kNegInf) {
+        // ln P(</s> | state) through the backoff chain; </s> is the last arc
+        // of a state's sorted arcs when present
+        float v = p.lm_unigram[V];
+        int found = -1;
+        float fv = 0.0f;
+#pragma unroll
+        for (int l = NL - 1; l >= 0; --l) {
+          const uint32_t n = lvc[h][l] & ~kExists;
+          if (found < 0 && n > 0) {
+            const LmArc a = p.lm_arcs[lvb[h][l] + n - 1];
+            if (a.token == static_cast<uint32_t>(V)) {
+              found = l;
+              fv = a.logp;
+            }
+          }
+        }
+        if (found >= 0) {
+          v = fv;
+#pragma unroll
+          for (int l = 0; l < NL; ++l)
+            if (l > found) v = v + lvbo[h][l];
+        } else {
+#pragma unroll
+          for (int l = 0; l < NL; ++l) v = v + lvbo[h][l];
+        }
+        const float av = alpha * v;
+        s = s + av;
+      }
+      if (HAS_BT && (p.flags & kFlagBoostRollback) && js < K && s != kNegInf) {
+        // the pending boosting of an unfinished phrase is taken back
+        const float wb = boost_w * static_cast<float>(-btpot[h]);
+        s = s + wb;
+      }
+      sj[h] = (js < K) ? s : kNegInf;
+    }
+    // rank of each slot: final score descending, lowest slot on ties
+    int rank[SPL];
+#pragma unroll
+    for (int h = 0; h < SPL; ++h) rank[h] = 0;
+    for (int i = 0; i < K; ++i) {
+      const float si = (i < 64) ? rdlane(sj[0], i) : rdlane(sj[SPL - 1], i & 63);
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) rank[h] += (si > sj[h] || (si == sj[h] && i < j + 64 * h)) ? 1 : 0;
+    }
+    int bj = 0;  // K >= 1: some slot has rank 0
+#pragma unroll
+    for (int h = SPL - 1; h >= 0; --h) {
+      const uint64_t top = __ballot(j + 64 * h < K && rank[h] == 0);
+      if (top) bj = static_cast<int>(__builtin_ctzll(top)) + 64 * h;
+    }
+    const float bs = (bj < 64) ? rdlane(sj[0], bj) : rdlane(sj[SPL - 1], bj & 63);
+    const int blen = (bj < 64) ? rdlane(len[0], bj) : rdlane(len[SPL - 1], bj & 63);
+#pragma unroll
+    for (int h = 0; h < SPL; ++h) {
+      const int js = j + 64 * h;
+      const int nlen = (js < K && sj[h] != kNegInf) ? len[h] : 0;
+      if (nbest && js < K) {
+        p.nbest_scores[static_cast<size_t>(b) * K + rank[h]] = sj[h];
+        p.nbest_lengths[static_cast<size_t>(b) * K + rank[h]] = nlen;
+        s_row[rank[h]] = static_cast<uint32_t>(nlen);  // lengths by rank (the row table is free now)
+        s_row[KMX + js] = static_cast<uint32_t>(rank[h]);
+      }
+    }
+    if (lane == 0) {
+      s_best = bj;
+      s_bestscore = bs;
+      s_bestlen = blen;
+    }
+    if (want_stats && lane == 0) {
+      // wave 0 made every update of s_st (LDS operations of one wave complete
+      // in order)
+      int64_t* so = p.stats + static_cast<size_t>(b) * 8;
+      so[0] = L;
+#pragma unroll
+      for (int q = 0; q < 6; ++q) so[1 + q] = static_cast<int64_t>(s_st[q]);
+      so[7] = 0;
+    }
+  }
+  __syncthreads();
+  const int best = s_best;
+  const float bscore = s_bestscore;
+  const bool have = bscore != kNegInf;
+  const int nout = have ? s_bestlen : 0;
+  int32_t* ot = p.out_tokens ? p.out_tokens + static_cast<size_t>(b) * T : nullptr;
+  if (ot)
+    for (int tt = nout + tid; tt < T; tt += kThreads) ot[tt] = -1;
+  if (tid == 0 && p.out_scores) {
+    p.out_scores[b] = bscore;
+    if (p.out_lengths) p.out_lengths[b] = nout;
+  }
+  int32_t* nbt = nbest ? p.nbest_tokens + static_cast<size_t>(b) * K * T : nullptr;
+  if (nbest) {
+    // padding of every row past its transcript
+    for (int r = 0; r < K; ++r) {
+      const int n = static_cast<int>(s_row[r]);
+      for (int tt = n + tid; tt < T; tt += kThreads) nbt[static_cast<size_t>(r) * T + tt] = -1;
+    }
+  }
+
+  // ---- traceback through the back-pointers, staged in LDS tiles ----
+  // 1-best: lane 0 of wave 0 walks the best slot.  N-best: lane j of wave 0
+  // walks slots j + 64 h (every live slot) and writes the rows of their ranks.
+  // (the LM.Final term is finite, so some slot is live exactly when the best
+  // final score is finite)
+  if (have && L > 0) {
+    const int tile_frames = kBigWords / K;
+    bool walker[SPL];
+    int jb[SPL], cnext[SPL], pos[SPL];
+    int32_t* orow[SPL];
+#pragma unroll
+    for (int h = 0; h < SPL; ++h) {
+      const int js = j + 64 * h;
+      walker[h] = (wave == 0) && (nbest ? (js < K && sc[h] != kNegInf) : (h == 0 && lane == 0));
+      jb[h] = nbest ? js : best;
+      cnext[h] = -1;
+      orow[h] = nullptr;
+      pos[h] = 0;
+      if (walker[h]) {
+        orow[h] = nbest ? nbt + static_cast<size_t>(s_row[KMX + js]) * T : ot;
+        pos[h] = nbest ? len[h] : nout;
+      }
+    }
+    for (int hi = L; hi > 0;) {
+      const int lo = hi > tile_frames ? hi - tile_frames : 0;
+      __syncthreads();
+      const int n = (hi - lo) * K;
+      const int32_t* src = bpb + static_cast<size_t>(lo) * K;
+      for (int q = tid; q < n; q += kThreads) s_big[q] = static_cast<uint32_t>(src[q]);
+      __syncthreads();
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        if (walker[h]) {
+          for (int tt = hi - 1; tt >= lo; --tt) {
+            const uint32_t e = s_big[(tt - lo) * K + jb[h]];
+            const int cl = static_cast<int>(e & 0xFFFFu);
+            const int par = static_cast<int>(e >> 16);
+            if (tt < L - 1 && cnext[h] != V && cnext[h] != cl) {
+              if (pos[h] > 0) {
+                --pos[h];
+                if (orow[h]) orow[h][pos[h]] = cnext[h];
+              }
+            }
+            cnext[h] = cl;
+            jb[h] = par;
+          }
+        }
+      }
+      hi = lo;
+    }
+    bool bad = false;
+#pragma unroll
+    for (int h = 0; h < SPL; ++h) {
+      if (walker[h]) {
+        if (cnext[h] != V && cnext[h] >= 0 && pos[h] > 0) {
+          --pos[h];
+          if (orow[h]) orow[h][pos[h]] = cnext[h];
+        }
+        bad = bad || pos[h] != 0;
+      }
+    }
+    if (wave == 0 && __ballot(bad) != 0ull) status |= 2u;
+  }
+  }
   if (tid == 0) p.status[b] = status;
 }
 
-template <int LPT, int NLEV>
+template <int LPT, int NLEV, int SPL>
 hipError_t launch_nlev(const KernelParams& p, hipStream_t s) {
   dim3 grid(p.B), block(kThreads);
   if (p.bt_nodes != nullptr)
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 
-template <int LPT>
-hipError_t launch_lpt_impl(const KernelParams& p, hipStream_t s) {
-  if (p.lm_states == nullptr && p.lm_arcs == nullptr) return launch_nlev<LPT, -1>(p, s);
+template <int LPT, int SPL>
+hipError_t launch_spl(const KernelParams& p, hipStream_t s) {
+  if (p.lm_states == nullptr && p.lm_arcs == nullptr) return launch_nlev<LPT, -1, SPL>(p, s);
   switch (p.lm_nlev) {
-    case 0: return launch_nlev<LPT, 0>(p, s);
-    case 1: return launch_nlev<LPT, 1>(p, s);
-    case 2: return launch_nlev<LPT, 2>(p, s);
-    case 3: return launch_nlev<LPT, 3>(p, s);
-    case 4: return launch_nlev<LPT, 4>(p, s);
-    case 5: return launch_nlev<LPT, 5>(p, s);
-    case 6: return launch_nlev<LPT, 6>(p, s);
-    case 7: return launch_nlev<LPT, 7>(p, s);
+    case 0: return launch_nlev<LPT, 0, SPL>(p, s);
+    case 1: return launch_nlev<LPT, 1, SPL>(p, s);
+    case 2: return launch_nlev<LPT, 2, SPL>(p, s);
+    case 3: return launch_nlev<LPT, 3, SPL>(p, s);
+    case 4: return launch_nlev<LPT, 4, SPL>(p, s);
+    case 5: return launch_nlev<LPT, 5, SPL>(p, s);
+    case 6: return launch_nlev<LPT, 6, SPL>(p, s);
+    case 7: return launch_nlev<LPT, 7, SPL>(p, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+// beams above 64 take two slots per lane (vocabularies of at most 1024
+// tokens; the host rejects the rest)
+template <int LPT>
+hipError_t launch_lpt_impl(const KernelParams& p, hipStream_t s) {
+  if constexpr (LPT <= 2) {
+    if (p.K > 64) return launch_spl<LPT, 2>(p, s);
+  } else {
+    if (p.K > 64) return hipErrorInvalidValue;
+  }
+  return launch_spl<LPT, 1>(p, s);
 }
 
 }  // namespace detail

@@ -612,6 +612,7 @@ size_t ctcbeam_workspace_bytes(int B, int T, int K) {
   return status_bytes(B) + static_cast<size_t>(B) * static_cast<size_t>(T) * static_cast<size_t>(K) * sizeof(int32_t);
 }
 
+static_assert(CTCBEAM_MAX_K == ctcbeam::kMaxK, "beam size limit");
 static_assert(CTCBEAM_FLAG_LOGSUMEXP == ctcbeam::kFlagLogSumExp, "flag values");
 static_assert(CTCBEAM_FLAG_BOOST_ROLLBACK == ctcbeam::kFlagBoostRollback, "flag values");
 
@@ -630,6 +631,8 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
   if (V > CTCBEAM_MAX_V) return fail(2, "V above " + std::to_string(CTCBEAM_MAX_V));
   if (K < 1) return fail(1, "K must be >= 1");
   if (K > CTCBEAM_MAX_K) return fail(2, "K above " + std::to_string(CTCBEAM_MAX_K));
+  if (!greedy && K > ctcbeam::kMaxKWideV && V > 1024)
+    return fail(2, "beams above " + std::to_string(ctcbeam::kMaxKWideV) + " need V <= 1024");
   if (static_cast<int64_t>(T) * (V + 1) >= (int64_t(1) << 40)) return fail(2, "T*(V+1) too large");
   if (lm && lm->V != V) return fail(1, "LM vocabulary size differs from V");
   if (boost && boost->V != V) return fail(1, "boosting tree vocabulary size differs from V");

@@ -283,6 +283,7 @@ def test_decode_rejects_bad_arguments_before_any_device_call():
 
     assert call(K=0) == 1
     assert call(K=P.MAX_K + 1) == 2
+    assert call(K=65, V=1025, ws_bytes=P.ctcbeam_workspace_bytes(2, 3, 65)) == 2  # wide V, K > 64
     assert call(V=0) == 1
     assert call(V=P.MAX_V + 1) == 2
     assert call(B=-1) == 1
