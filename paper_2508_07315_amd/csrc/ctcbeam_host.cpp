@@ -21,6 +21,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -30,6 +31,8 @@
 #include <new>
 #include <sstream>
 #include <string>
+#include <string_view>
+#include <thread>
 #include <unordered_map>
 #include <vector>
 
@@ -81,6 +84,51 @@ float log10_to_ln(float v) {
 }
 
 // Sorted n-gram rows of one order.
+// ---- host-side parallelism for the table builders (results do not depend
+// on the thread count) ----
+int host_threads() {
+  const unsigned h = std::thread::hardware_concurrency();
+  return static_cast<int>(std::max(1u, std::min(h ? h : 1u, 16u)));
+}
+// f(begin, end) over contiguous parts of [0, n)
+template <class F>
+void parallel_for(int64_t n, F&& f, int64_t grain = 65536) {
+  const int64_t P = std::min<int64_t>(host_threads(), std::max<int64_t>(1, n / grain));
+  if (P <= 1) {
+    f(int64_t(0), n);
+    return;
+  }
+  std::vector<std::thread> th;
+  for (int64_t t = 0; t < P; ++t) th.emplace_back([&f, n, t, P]() { f(n * t / P, n * (t + 1) / P); });
+  for (auto& x : th) x.join();
+}
+// sort by a total order: parts sorted in parallel, then merged pairwise
+template <class T, class Cmp>
+void parallel_sort(std::vector<T>& v, Cmp cmp) {
+  const int64_t n = static_cast<int64_t>(v.size());
+  int64_t P = 1;
+  while (P * 2 <= host_threads() && n / (P * 2) >= 65536) P *= 2;
+  if (P <= 1) {
+    std::sort(v.begin(), v.end(), cmp);
+    return;
+  }
+  std::vector<int64_t> b(P + 1);
+  for (int64_t t = 0; t <= P; ++t) b[t] = n * t / P;
+  {
+    std::vector<std::thread> th;
+    for (int64_t t = 0; t < P; ++t) th.emplace_back([&, t]() { std::sort(v.begin() + b[t], v.begin() + b[t + 1], cmp); });
+    for (auto& x : th) x.join();
+  }
+  for (int64_t w = 1; w < P; w *= 2) {
+    std::vector<std::thread> th;
+    for (int64_t t = 0; t + w < P; t += 2 * w)
+      th.emplace_back([&, t, w]() {
+        std::inplace_merge(v.begin() + b[t], v.begin() + b[t + w], v.begin() + b[std::min(t + 2 * w, P)], cmp);
+      });
+    for (auto& x : th) x.join();
+  }
+}
+
 struct Order {
   int m = 0;
   int64_t n = 0;
@@ -165,16 +213,27 @@ int build_lm_tables(int order, int V, const int64_t* counts, const int32_t* cons
     if (o.n >= (int64_t(1) << 31)) return fail(2, "too many n-grams of one order");
     const int32_t* src = ngram_ids[m - 1];
     std::vector<int64_t> perm(o.n);
-    for (int64_t i = 0; i < o.n; ++i) {
-      perm[i] = i;
-      const int32_t* r = src + i * m;
-      for (int j = 0; j < m; ++j) {
-        if (r[j] < 0 || r[j] > BOS) return fail(1, "n-gram id out of range");
-        if (r[j] == BOS && j != 0) return fail(1, "<s> may only start an n-gram");
-        if (r[j] == EOS && j != m - 1) return fail(1, "</s> may only end an n-gram");
+    std::atomic<int> bad{0};  // 1 id range, 2 <s> position, 3 </s> position
+    parallel_for(o.n, [&](int64_t lo, int64_t hi) {
+      for (int64_t i = lo; i < hi; ++i) {
+        perm[i] = i;
+        const int32_t* r = src + i * m;
+        for (int j = 0; j < m; ++j) {
+          int e = 0;
+          if (r[j] < 0 || r[j] > BOS) e = 1;
+          else if (r[j] == BOS && j != 0) e = 2;
+          else if (r[j] == EOS && j != m - 1) e = 3;
+          if (e) {
+            int z = 0;
+            bad.compare_exchange_strong(z, e);
+          }
+        }
       }
-    }
-    std::sort(perm.begin(), perm.end(), [src, m](int64_t a, int64_t b) {
+    });
+    if (bad == 1) return fail(1, "n-gram id out of range");
+    if (bad == 2) return fail(1, "<s> may only start an n-gram");
+    if (bad == 3) return fail(1, "</s> may only end an n-gram");
+    parallel_sort(perm, [src, m](int64_t a, int64_t b) {
       const int32_t* ra = src + a * m;
       const int32_t* rb = src + b * m;
       for (int j = 0; j < m; ++j)
@@ -185,14 +244,21 @@ int build_lm_tables(int order, int V, const int64_t* counts, const int32_t* cons
     o.lnp.resize(o.n);
     o.lnbo.assign(o.n, 0.0f);
     const float* bo = (m < order && log10_bow) ? log10_bow[m - 1] : nullptr;
-    for (int64_t i = 0; i < o.n; ++i) {
-      const int64_t s = perm[i];
-      std::memcpy(&o.ids[i * m], src + s * m, sizeof(int32_t) * m);
-      o.lnp[i] = log10_to_ln(log10_prob[m - 1][s]);
-      if (bo && src[s * m + m - 1] != EOS) o.lnbo[i] = log10_to_ln(bo[s]);
-      if (i > 0 && std::memcmp(&o.ids[(i - 1) * m], &o.ids[i * m], sizeof(int32_t) * m) == 0)
-        return fail(1, "duplicate " + std::to_string(m) + "-gram");
-    }
+    const float* pr = log10_prob[m - 1];
+    parallel_for(o.n, [&](int64_t lo, int64_t hi) {
+      for (int64_t i = lo; i < hi; ++i) {
+        const int64_t s = perm[i];
+        std::memcpy(&o.ids[i * m], src + s * m, sizeof(int32_t) * m);
+        o.lnp[i] = log10_to_ln(pr[s]);
+        if (bo && src[s * m + m - 1] != EOS) o.lnbo[i] = log10_to_ln(bo[s]);
+      }
+    });
+    std::atomic<bool> dup{false};
+    parallel_for(o.n, [&](int64_t lo, int64_t hi) {
+      for (int64_t i = std::max<int64_t>(lo, 1); i < hi; ++i)
+        if (std::memcmp(&o.ids[(i - 1) * m], &o.ids[i * m], sizeof(int32_t) * m) == 0) dup = true;
+    });
+    if (dup) return fail(1, "duplicate " + std::to_string(m) + "-gram");
   }
   // every token and </s> needs a unigram
   lm->unigram.assign(V + 1, 0.0f);
@@ -204,11 +270,14 @@ int build_lm_tables(int order, int V, const int64_t* counts, const int32_t* cons
   // prefix closure
   for (int m = 2; m <= order; ++m) {
     const Order& o = ord[m];
-    for (int64_t i = 0; i < o.n; ++i) {
-      if (i > 0 && std::memcmp(o.row(i - 1), o.row(i), sizeof(int32_t) * (m - 1)) == 0) continue;
-      if (ord[m - 1].find(o.row(i)) < 0)
-        return fail(1, "an " + std::to_string(m) + "-gram's context is not an entry (model not prefix-closed)");
-    }
+    std::atomic<bool> open{false};
+    parallel_for(o.n, [&](int64_t lo, int64_t hi) {
+      for (int64_t i = lo; i < hi; ++i) {
+        if (i > 0 && std::memcmp(o.row(i - 1), o.row(i), sizeof(int32_t) * (m - 1)) == 0) continue;
+        if (ord[m - 1].find(o.row(i)) < 0) open = true;
+      }
+    });
+    if (open) return fail(1, "an " + std::to_string(m) + "-gram's context is not an entry (model not prefix-closed)");
   }
   // states
   const int nlev = order - 1;
@@ -246,12 +315,18 @@ int build_lm_tables(int order, int V, const int64_t* counts, const int32_t* cons
     }
   }
   lm->arcs.resize(n_arcs);
-  std::vector<int32_t> tmp(order + 1);
   for (int m = 2; m <= order; ++m) {
     const Order& o = ord[m];
     const Order& ctx = ord[m - 1];
-    int64_t i = 0;
-    while (i < o.n) {
+    // parts start at the first row of a context group, so no group is split
+    auto group_start = [&](int64_t i) {
+      while (i > 0 && i < o.n && std::memcmp(o.row(i - 1), o.row(i), sizeof(int32_t) * (m - 1)) == 0) ++i;
+      return std::min(i, o.n);
+    };
+    parallel_for(o.n, [&](int64_t lo0, int64_t hi0) {
+    const int64_t lo = group_start(lo0), hi = group_start(hi0);
+    int64_t i = lo;
+    while (i < hi) {
       int64_t j = i + 1;
       while (j < o.n && std::memcmp(o.row(i), o.row(j), sizeof(int32_t) * (m - 1)) == 0) ++j;
       const int64_t ci = ctx.find(o.row(i));
@@ -276,13 +351,16 @@ int build_lm_tables(int order, int V, const int64_t* counts, const int32_t* cons
       }
       i = j;
     }
+    });
   }
   // chain records
   lm->states.assign(static_cast<size_t>(n_states) * nlev, LmLevel{0, 0, 0.0f});
-  uint32_t max_chain = 0;
+  std::atomic<uint32_t> max_chain_a{0};
   for (int m = 1; m < order; ++m) {
     const Order& o = ord[m];
-    for (int64_t i = 0; i < o.n; ++i) {
+    parallel_for(o.n, [&](int64_t lo, int64_t hi) {
+    uint32_t part_max = 0;
+    for (int64_t i = lo; i < hi; ++i) {
       const uint32_t s = o.state[i];
       if (s == UINT32_MAX) continue;
       const int32_t* h = o.row(i);
@@ -298,9 +376,14 @@ int build_lm_tables(int order, int V, const int64_t* counts, const int32_t* cons
         rec.bo = sbo[u];
         chain += scnt[u];
       }
-      max_chain = std::max(max_chain, chain);
+      part_max = std::max(part_max, chain);
     }
+    uint32_t cur = max_chain_a.load();
+    while (part_max > cur && !max_chain_a.compare_exchange_weak(cur, part_max)) {
+    }
+    });
   }
+  const uint32_t max_chain = max_chain_a.load();
   if (max_chain > static_cast<uint32_t>(ctcbeam::kLmStage))
     return fail(2, "a backoff chain holds " + std::to_string(max_chain) +
                        " explicit continuations (limit " + std::to_string(ctcbeam::kLmStage) + ")");
@@ -487,60 +570,160 @@ int lm_build_arpa(const char* path, int vocab_size, bool device, ctcbeam_lm** ou
   *out = nullptr;
   if (!path) return fail(1, "null path");
   if (vocab_size < 1) return fail(1, "vocab_size must be >= 1");
-  std::ifstream in(path);
-  if (!in) return fail(1, std::string("cannot open ") + path);
-  std::vector<std::vector<int32_t>> ids;
-  std::vector<std::vector<float>> lp, lb;
-  int cur = 0;
-  std::string line;
-  auto word_id = [vocab_size](const std::string& w, int32_t* id) {
-    if (w == "</s>") { *id = vocab_size; return true; }
-    if (w == "<s>") { *id = vocab_size + 1; return true; }
-    if (w.empty() || w.size() > 9) return false;
+  // the whole file in memory, NUL-terminated
+  std::vector<char> buf;
+  {
+    std::FILE* f = std::fopen(path, "rb");
+    if (!f) return fail(1, std::string("cannot open ") + path);
+    std::fseek(f, 0, SEEK_END);
+    const long sz = std::ftell(f);
+    std::fseek(f, 0, SEEK_SET);
+    buf.resize(static_cast<size_t>(sz > 0 ? sz : 0) + 1);
+    const size_t got = sz > 0 ? std::fread(buf.data(), 1, static_cast<size_t>(sz), f) : 0;
+    std::fclose(f);
+    buf.resize(got + 1);
+    buf[got] = '\0';
+  }
+  const char* const base = buf.data();
+  const char* const fend = base + buf.size() - 1;
+  // one line [p, e) without its CR
+  auto next_line = [fend](const char* p, const char** e, const char** nxt) {
+    const char* q = static_cast<const char*>(std::memchr(p, '\n', static_cast<size_t>(fend - p)));
+    const char* le = q ? q : fend;
+    *nxt = q ? q + 1 : fend;
+    if (le > p && le[-1] == '\r') --le;
+    *e = le;
+  };
+  // pass 1: the data lines of each order, as byte ranges
+  std::vector<std::pair<const char*, const char*>> sect;  // by order - 1
+  {
+    int cur = 0;
+    const char* p = base;
+    const char* sec_begin = nullptr;
+    while (p < fend) {
+      const char *e, *nxt;
+      next_line(p, &e, &nxt);
+      const std::string_view line(p, static_cast<size_t>(e - p));
+      if (!line.empty() && line[0] == '\\') {
+        if (cur > 0) sect[cur - 1] = {sec_begin, p};
+        cur = 0;
+        if (line == "\\end\\") break;
+        if (line != "\\data\\") {
+          const int m = std::atoi(std::string(line.substr(1)).c_str());
+          if (m < 1 || m > static_cast<int>(sect.size())) return fail(1, "ARPA section without a header count");
+          cur = m;
+          sec_begin = nxt;
+        }
+      } else if (cur == 0 && line.rfind("ngram ", 0) == 0) {
+        const int m = std::atoi(std::string(line.substr(6)).c_str());
+        if (m < 1 || m > CTCBEAM_MAX_ORDER) return fail(m < 1 ? 1 : 2, "bad ngram order in ARPA header");
+        if (static_cast<int>(sect.size()) < m) sect.resize(m, {nullptr, nullptr});
+      }
+      p = nxt;
+    }
+    if (cur > 0) sect[cur - 1] = {sec_begin, p};
+  }
+  auto word_id = [vocab_size](const char* w, size_t n, int32_t* id) {
+    if (n == 4 && std::memcmp(w, "</s>", 4) == 0) { *id = vocab_size; return true; }
+    if (n == 3 && std::memcmp(w, "<s>", 3) == 0) { *id = vocab_size + 1; return true; }
+    if (n == 0 || n > 9) return false;
     int32_t v = 0;
-    for (char ch : w) {
-      if (ch < '0' || ch > '9') return false;
-      v = v * 10 + (ch - '0');
+    for (size_t i = 0; i < n; ++i) {
+      if (w[i] < '0' || w[i] > '9') return false;
+      v = v * 10 + (w[i] - '0');
     }
     if (v >= vocab_size) return false;
     *id = v;
     return true;
   };
-  while (std::getline(in, line)) {
-    if (!line.empty() && line.back() == '\r') line.pop_back();
-    if (line.empty()) continue;
-    if (line == "\\data\\") { cur = 0; continue; }
-    if (line == "\\end\\") break;
-    if (line.rfind("ngram ", 0) == 0) {
-      const int m = std::atoi(line.c_str() + 6);
-      if (m < 1 || m > CTCBEAM_MAX_ORDER) return fail(m < 1 ? 1 : 2, "bad ngram order in ARPA header");
-      if (static_cast<int>(ids.size()) < m) {
-        ids.resize(m);
-        lp.resize(m);
-        lb.resize(m);
+  auto is_space = [](char c) { return c == ' ' || c == '\t' || c == '\v' || c == '\f'; };
+  // pass 2: each order's lines parsed in parts (split at line starts), then
+  // joined in file order
+  std::vector<std::vector<int32_t>> ids(sect.size());
+  std::vector<std::vector<float>> lp(sect.size()), lb(sect.size());
+  for (size_t mi = 0; mi < sect.size(); ++mi) {
+    const int cur = static_cast<int>(mi) + 1;
+    const char* sb = sect[mi].first;
+    const char* se = sect[mi].second;
+    if (!sb || se <= sb) continue;
+    const int64_t nbytes = se - sb;
+    const int P = static_cast<int>(std::min<int64_t>(host_threads(), std::max<int64_t>(1, nbytes / (1 << 20))));
+    struct Part {
+      std::vector<int32_t> ids;
+      std::vector<float> lp, lb;
+      const char* bad = nullptr;  // first malformed line
+    };
+    std::vector<Part> parts(P);
+    std::vector<const char*> cut(P + 1);
+    cut[0] = sb;
+    cut[P] = se;
+    for (int t = 1; t < P; ++t) {
+      const char* q = sb + nbytes * t / P;
+      const char* nl = static_cast<const char*>(std::memchr(q, '\n', static_cast<size_t>(se - q)));
+      cut[t] = nl ? nl + 1 : se;
+      if (cut[t] < cut[t - 1]) cut[t] = cut[t - 1];
+    }
+    auto parse = [&](int t) {
+      Part& pt = parts[t];
+      const char* p = cut[t];
+      int32_t g[CTCBEAM_MAX_ORDER];
+      const char* tok[CTCBEAM_MAX_ORDER + 2];
+      size_t tlen[CTCBEAM_MAX_ORDER + 2];
+      while (p < cut[t + 1]) {
+        const char *e, *nxt;
+        next_line(p, &e, &nxt);
+        int nt = 0;
+        for (const char* q = p; q < e && nt < cur + 2;) {
+          while (q < e && is_space(*q)) ++q;
+          if (q >= e) break;
+          const char* w = q;
+          while (q < e && !is_space(*q)) ++q;
+          tok[nt] = w;
+          tlen[nt] = static_cast<size_t>(q - w);
+          ++nt;
+        }
+        if (nt == 0) {  // empty line
+          p = nxt;
+          continue;
+        }
+        if (nt < cur + 1) {
+          if (!pt.bad) pt.bad = p;
+          p = nxt;
+          continue;
+        }
+        bool ok = true;
+        for (int j = 0; j < cur; ++j) ok = ok && word_id(tok[1 + j], tlen[1 + j], &g[j]);
+        if (ok) {  // n-grams with an unknown word are skipped
+          pt.ids.insert(pt.ids.end(), g, g + cur);
+          pt.lp.push_back(std::strtof(tok[0], nullptr));
+          pt.lb.push_back(nt > cur + 1 ? std::strtof(tok[cur + 1], nullptr) : 0.0f);
+        }
+        p = nxt;
       }
-      continue;
+    };
+    {
+      std::vector<std::thread> th;
+      for (int t = 1; t < P; ++t) th.emplace_back(parse, t);
+      parse(0);
+      for (auto& x : th) x.join();
     }
-    if (line[0] == '\\') {
-      const int m = std::atoi(line.c_str() + 1);
-      if (m < 1 || m > static_cast<int>(ids.size())) return fail(1, "ARPA section without a header count");
-      cur = m;
-      continue;
+    for (int t = 0; t < P; ++t) {
+      if (parts[t].bad) {
+        const char *e, *nxt;
+        next_line(parts[t].bad, &e, &nxt);
+        return fail(1, "malformed ARPA line: " + std::string(parts[t].bad, static_cast<size_t>(e - parts[t].bad)));
+      }
     }
-    if (cur == 0) continue;
-    std::istringstream ss(line);
-    std::string tok;
-    std::vector<std::string> parts;
-    while (ss >> tok) parts.push_back(tok);
-    if (static_cast<int>(parts.size()) < cur + 1) return fail(1, "malformed ARPA line: " + line);
-    std::vector<int32_t> g(cur);
-    bool ok = true;
-    for (int j = 0; j < cur; ++j) ok = ok && word_id(parts[1 + j], &g[j]);
-    if (!ok) continue;  // n-gram with an unknown word
-    ids[cur - 1].insert(ids[cur - 1].end(), g.begin(), g.end());
-    lp[cur - 1].push_back(std::strtof(parts[0].c_str(), nullptr));
-    lb[cur - 1].push_back(static_cast<int>(parts.size()) > cur + 1 ? std::strtof(parts[cur + 1].c_str(), nullptr)
-                                                                   : 0.0f);
+    size_t n = 0;
+    for (const Part& pt : parts) n += pt.lp.size();
+    ids[mi].reserve(n * cur);
+    lp[mi].reserve(n);
+    lb[mi].reserve(n);
+    for (const Part& pt : parts) {
+      ids[mi].insert(ids[mi].end(), pt.ids.begin(), pt.ids.end());
+      lp[mi].insert(lp[mi].end(), pt.lp.begin(), pt.lp.end());
+      lb[mi].insert(lb[mi].end(), pt.lb.begin(), pt.lb.end());
+    }
   }
   const int order = static_cast<int>(ids.size());
   if (order == 0) return fail(1, "no n-grams in ARPA file");

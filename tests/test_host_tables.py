@@ -145,6 +145,48 @@ def test_arpa_builder_matches_arrays():
             assert walker.value(walker.state(y), c) == F32(ref.score(y, c))
 
 
+def test_arpa_reader_formatting_and_errors(tmp_path):
+    """The ARPA reader takes CRLF line ends, blank lines, tabs and skips
+    n-grams with a word outside the vocabulary; a line with too few fields
+    is an error.  A large file is parsed in parallel parts and still equals
+    the array build."""
+    V = 40
+    arrays = W.make_lm(3, V, [600, 900], 77)
+    clean = tmp_path / "clean.arpa"
+    W.write_arpa(arrays, str(clean))
+    text = clean.read_text()
+    lines = text.split("\n")
+    messy = []
+    for i, ln in enumerate(lines):
+        if ln and ln[0] not in "\\n" and i % 7 == 0:
+            ln = ln.replace(" ", "\t", 1)
+        messy.append(ln + ("\r" if i % 3 == 0 else ""))
+        if i % 11 == 0:
+            messy.append("")
+    # an n-gram with an unknown word, inside the 2-gram section
+    k = next(i for i, ln in enumerate(messy) if ln.rstrip("\r") == "\\2-grams:")
+    messy.insert(k + 1, "-1.5 99999 3 -0.2")
+    path = tmp_path / "messy.arpa"
+    path.write_text("\n".join(messy))
+    a = P.ctcbeam_lm_tables(P.ctcbeam_lm_build_arpa_host(str(path), V))
+    b = P.ctcbeam_lm_tables(P.ctcbeam_lm_build_host(arrays))
+    for key in ("states", "arcs", "unigram"):
+        np.testing.assert_array_equal(a[key], b[key])
+    bad = tmp_path / "bad.arpa"
+    bad.write_text(text.replace("\\2-grams:\n", "\\2-grams:\n-1.0 5\n", 1))
+    with pytest.raises(P.CtcbeamError) as e:
+        P.ctcbeam_lm_build_arpa_host(str(bad), V)
+    assert e.value.code == 1 and "malformed" in str(e.value)
+    # several MB: parsed in parts, identical to the array build
+    big = W.make_lm(3, 1024, [60000, 150000], 78)
+    bigp = tmp_path / "big.arpa"
+    W.write_arpa(big, str(bigp))
+    a = P.ctcbeam_lm_tables(P.ctcbeam_lm_build_arpa_host(str(bigp), 1024))
+    b = P.ctcbeam_lm_tables(P.ctcbeam_lm_build_host(big))
+    for key in ("states", "arcs", "unigram"):
+        np.testing.assert_array_equal(a[key], b[key])
+
+
 # ---------------------------------------------------------------------------
 # Boosting tables
 # ---------------------------------------------------------------------------
