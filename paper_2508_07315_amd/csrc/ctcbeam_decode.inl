@@ -359,9 +359,6 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   const int kcmax = min(K, KSEG);
   const float alpha = p.alpha, beta = p.beta, boost_w = p.boost_w;
   const uint64_t lmlt = lanemask_lt();
-  // lanes <= this lane, as two 32-bit halves
-  const uint32_t lmle_lo = lane >= 31 ? 0xFFFFFFFFu : ((2u << lane) - 1u);
-  const uint32_t lmle_hi = lane < 32 ? 0u : (lane == 63 ? 0xFFFFFFFFu : ((2u << (lane - 32)) - 1u));
 
   int L = p.lengths[b];
   uint32_t status = 0;

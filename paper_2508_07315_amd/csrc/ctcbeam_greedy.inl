@@ -79,7 +79,6 @@ __device__ __forceinline__ int wave_min(int v) {
 
 // four consecutive fp32 at a 4-byte aligned address (one dwordx4 access)
 typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));
-typedef float f4a __attribute__((ext_vector_type(4), aligned(16)));
 
 // Label of a lane's r-th slot: lanes own runs of 4 consecutive labels, runs of
 // the wave are 256 labels apart, so a frame row is read with dwordx4 loads

@@ -10,8 +10,6 @@ constexpr int kThreads = 512;         // threads per workgroup (8 wave64)
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxK = 128;            // beam size limit
 constexpr int kMaxKWideV = 64;        // beam size limit above 1024 tokens
-constexpr int kMaxLev = 7;            // LM order - 1 limit
-constexpr int kKeyWords = 8192;       // per-chunk [hyp][token] key row entries
 constexpr int kLmStage = 4096;        // staged LM arcs per chunk (12-bit slot)
 constexpr int kCap = 512;             // survivor pool entries
 constexpr uint32_t kExists = 0x80000000u;
