@@ -293,6 +293,45 @@ __device__ __forceinline__ bool recomb_shifts(uint32_t klo, uint32_t khi) {
   return m;
 }
 
+// Bitonic sort of (hi, lo, slot) triples, one per lane, ascending over the
+// wave (slots are distinct, so the order is total).
+template <int k, int jd>
+__device__ __forceinline__ void sort3_step(uint32_t& lo, uint32_t& hi, uint32_t& sl, int lane) {
+  const uint32_t olo = xor_lane(lo, jd, lane), ohi = xor_lane(hi, jd, lane), osl = xor_lane(sl, jd, lane);
+  const bool less = ohi < hi || (ohi == hi && (olo < lo || (olo == lo && osl < sl)));
+  // lanes that keep the larger in the descending network keep the smaller here
+  const bool take = less == lane_in_here<bitonic_max_lanes(k, jd, 64)>();
+  lo = take ? olo : lo;
+  hi = take ? ohi : hi;
+  sl = take ? osl : sl;
+}
+template <int k, int jd>
+__device__ __forceinline__ void sort3_merge(uint32_t& lo, uint32_t& hi, uint32_t& sl, int lane) {
+  sort3_step<k, jd>(lo, hi, sl, lane);
+  if constexpr (jd > 1) sort3_merge<k, jd / 2>(lo, hi, sl, lane);
+}
+template <int k>
+__device__ __forceinline__ void sort3_levels(uint32_t& lo, uint32_t& hi, uint32_t& sl, int lane) {
+  sort3_merge<k, k / 2>(lo, hi, sl, lane);
+  if constexpr (k < 64) sort3_levels<k * 2>(lo, hi, sl, lane);
+}
+// Recombination of up to 64 slots (lane = slot): sorts the 64-bit keys with
+// their slots and flags each slot whose sorted predecessor has the same key,
+// i.e. a lower slot with the same transcript.  Dead slots carry all ones and
+// are never flagged.  The sorted keys are left in lo / hi (for searches).
+__device__ __forceinline__ bool dup_by_sort(uint64_t key, int lane, uint32_t& lo, uint32_t& hi) {
+  lo = static_cast<uint32_t>(key);
+  hi = static_cast<uint32_t>(key >> 32);
+  uint32_t sl = static_cast<uint32_t>(lane);
+  sort3_levels<2>(lo, hi, sl, lane);
+  const int pa = (lane == 0 ? 63 : lane - 1) << 2;
+  const uint32_t plo = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(pa, static_cast<int>(lo)));
+  const uint32_t phi = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(pa, static_cast<int>(hi)));
+  const bool d = lane > 0 && plo == lo && phi == hi && (lo & hi) != 0xFFFFFFFFu;
+  // back to the slot's lane (the slots are a permutation of the lanes)
+  return __builtin_amdgcn_ds_permute(static_cast<int>(sl) << 2, d ? 1 : 0) != 0;
+}
+
 // Bitonic sort of one value per lane within groups of N lanes, descending.
 template <int N>
 __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
@@ -300,8 +339,10 @@ __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
 }
 
 // SPL = beam slots per lane: slot j lives in lane j % 64, register set
-// j / 64 (SPL = 2 serves beams of 65..128).
-template <int LPT, int NLEV, bool HAS_BT, int SPL>
+// j / 64 (SPL = 2 serves beams of 65..128).  SKIP: ranks of chunks before
+// the last are skipped while the survivor pool has room (beams above one
+// chunk; small beams keep one rank per chunk and the simpler code).
+template <int LPT, int NLEV, bool HAS_BT, int SPL, bool SKIP>
 __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool HAS_LM = NLEV >= 0;
   constexpr int NL = NLEV > 0 ? NLEV : 0;     // chain levels above the unigram root
@@ -332,6 +373,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   __shared__ __align__(16) uint32_t s_big[kBigWords];
   // survivor pool: score bits, flat index, LM target (raw), boosting key
   __shared__ uint4 s_pool[kCap];
+  static_assert(kCap / 2 <= kThreads, "the fallback reads carried pool entries one per thread");
   // reserved regions (ping-pong): blank candidates, or the best K so far
   __shared__ uint4 s_res[2][KMX];
   // beam records by live position: score, last label, slot, pot, backoff weights
@@ -578,6 +620,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     }
     float tau_run = kNegInf;
     int nfin = 0;
+    // survivors carried in the pool from chunks whose rank was skipped
+    int carry = 0;
     int cs = 0;  // live position of the chunk's first beam
 
     for (int ch = 0; ch < nch; ++ch) {
@@ -853,7 +897,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           }
         }
       }
-      if (tid == 0) {
+      if (tid == 0 && carry == 0) {
         s_nbuf = 0;  // the previous rank read it before barrier D
         s_overflow = 0;
       }
@@ -946,8 +990,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               if (slot < kCap) {
                 const int i = r / LPT, jj = r % LPT;
                 const int c = tid + jj * kThreads;
-                // LM target: staged entry (resolved by the rank) or the
-                // token's unigram state
+                // LM target: the staged arc's or the token's unigram state.
+                // With rank skipping it is resolved now (a later chunk reuses
+                // the staging area before the rank), otherwise by the rank.
                 uint32_t lraw, bk;
                 if constexpr (kKeepLm) {
                   lraw = lhi[r];
@@ -955,6 +1000,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                 } else {
                   cand_meta(i, jj, lraw, bk);
                 }
+                if (HAS_LM && SKIP && (lraw >> kGenShift) != 0u) lraw = tgt[lraw & 0xFFFu];
                 s_pool[slot] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lraw, bk);
               } else {
                 s_overflow = 1;
@@ -968,10 +1014,19 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 
       // ---- R. exact rank of the pool: reserved region P + survivors ----
       // The best K go to region Q in rank order; after the last chunk the
-      // winners' successor records go to s_rec[rcur ^ 1] instead.
+      // winners' successor records go to s_rec[rcur ^ 1] instead.  Before
+      // the last chunk the rank runs only when the pool is more than half
+      // full (or overflowed): otherwise the survivors stay in the pool for
+      // the next chunk (with large beams most chunks skip it).
+      const bool last_chunk = ch + 1 == nch;
+      const int npool = s_nbuf;
+      if (SKIP && !last_chunk && !s_overflow && npool <= kCap / 2) {  // uniform
+        carry = npool;
+        cs += kc;
+        continue;
+      }
       {
         const int P = mpar, Q = mpar ^ 1;
-        const bool last_chunk = ch + 1 == nch;
         const uint32_t* prec = s_rec + rcur * (KMX * RW);
         uint32_t* nrec = s_rec + (rcur ^ 1) * (KMX * RW);
         if (!s_overflow) {
@@ -986,7 +1041,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             nfin = __popcll(__ballot(xq != kNegInf));
             const bool own = ((lane & (kWaves - 1)) == wave) && xq != kNegInf;
             uint32_t lmt = eq.z;
-            if (HAS_LM && lane >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+            if (HAS_LM && !SKIP && lane >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
             Succ sp;
             if (last_chunk) succ_begin(own, eq.y, lmt, eq.w, prec, sp);  // loads overlap the ranking
             int myrank = K;
@@ -1042,7 +1097,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               for (int u = 0; u < 8; ++u) myrank = ((lane >> 3) == u) ? rk[u] : myrank;
               const bool win = (lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf;
               uint32_t lmt = eq.z;
-              if (HAS_LM && win && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+              if (HAS_LM && !SKIP && win && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
               if (last_chunk) {
                 Succ sp;
                 succ_begin(win, eq.y, lmt, eq.w, prec, sp);
@@ -1054,12 +1109,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
           }
         } else {
-          // exact extraction over (reserved region P) U (this chunk's candidates)
+          // exact extraction over (reserved region P) U (pool entries carried
+          // from earlier chunks) U (this chunk's candidates)
           uint64_t prev = ~0ull;
           int nk = 0;
           for (int it = 0; it < K; ++it) {
             uint64_t best = 0ull;
-            int who = -1;  // -1 none, 0 a register candidate, 100+e reserved entry
+            int who = -1;  // -1 none, 0 a register candidate, 100+e reserved, 1000+e pool entry
             // the best register candidate's fields, tracked by selects so that
             // no candidate array is indexed at run time
             float wx = kNegInf;
@@ -1092,6 +1148,17 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                 }
               }
             }
+            if (tid < carry) {  // carry <= kCap / 2 <= kThreads
+              const uint4 e = s_pool[tid];
+              const float xe = __uint_as_float(e.x);
+              if (xe != kNegInf) {
+                const uint64_t key = order_key(xe, e.y);
+                if (key < prev && key > best) {
+                  best = key;
+                  who = 1000 + tid;
+                }
+              }
+            }
             uint64_t wbest = best;
             for (int off = 1; off < 64; off <<= 1) {
               const uint64_t o = __shfl_xor(wbest, off);
@@ -1118,8 +1185,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   bk = (be >= genhi) ? be : p.bt_root_key[c];
                 }
                 s_res[Q][it] = make_uint4(__float_as_uint(wx), wflat, lmt, bk);
-              } else {
+              } else if (who < 1000) {
                 s_res[Q][it] = s_res[P][who - 100];
+              } else {
+                s_res[Q][it] = s_pool[who - 1000];
               }
             }
             prev = gbest;
@@ -1144,6 +1213,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       }
       __syncthreads();  // D: best K of the chunk in region Q
       mpar ^= 1;
+      carry = 0;
       if (ch + 1 < nch && nfin >= K) tau_run = fmaxf(tau_run, __uint_as_float(s_res[mpar][K - 1].x));
       cs += kc;
     }
@@ -1186,15 +1256,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         const uint32_t klo = static_cast<uint32_t>(key), khi = static_cast<uint32_t>(key >> 32);
         dup = (K <= 8 ? recomb_shifts<1, 7>(klo, khi) : recomb_shifts<1, 15>(klo, khi)) && alive0;
       } else {
-        uint64_t mr = __ballot(alive0) & ~(1ull << 63);  // the top lane is never the lower slot
-        while (mr) {
-          const int i = static_cast<int>(__builtin_ctzll(mr));
-          mr &= mr - 1ull;
-          const uint32_t hlo = rdlane(rec[kRHlo], i);
-          const uint32_t hhi = rdlane(rec[kRHhi], i);
-          const uint32_t mi = rdlane(meta, i);
-          dup = dup || (j > i && alive0 && rec[kRHlo] == hlo && rec[kRHhi] == hhi && meta == mi);
-        }
+        // the same key, compared through a sort of all 64 slots
+        uint64_t key = ((static_cast<uint64_t>(rec[kRHhi]) << 32) | rec[kRHlo]) ^
+                       (static_cast<uint64_t>(meta + 1u) * 0xD6E8FEB86659FD93ull);
+        if (!alive0) key = ~0ull;
+        uint32_t slo, shi;
+        dup = dup_by_sort(key, lane, slo, shi) && alive0;
       }
       if (p.flags & kFlagLogSumExp) {  // uniform
         // Each duplicate, in slot order, is merged into the first live slot
@@ -1338,22 +1405,35 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         const uint32_t klo = static_cast<uint32_t>(key), khi = static_cast<uint32_t>(key >> 32);
         dup[0] = (K <= 8 ? recomb_shifts<1, 7>(klo, khi) : recomb_shifts<1, 15>(klo, khi)) && alive0[0];
       } else {
-        // every live slot i against the slots above it, in slot order
+        // Each register set is sorted on its own (its slots are in lane
+        // order); a slot of the upper set is also a duplicate when its key
+        // occurs among the live keys of the lower set (all lower slots):
+        // binary search in the lower set's sorted keys.
+        uint64_t key[SPL];
+        uint32_t slo[SPL], shi[SPL];
 #pragma unroll
-        for (int hi = 0; hi < SPL; ++hi) {
-          uint64_t mr = __ballot(alive0[hi]);
-          if (hi == SPL - 1) mr &= ~(1ull << 63);  // the top slot is never the lower one
-          while (mr) {
-            const int i = static_cast<int>(__builtin_ctzll(mr));
-            mr &= mr - 1ull;
-            const uint32_t hlo = rdlane(rec[hi][kRHlo], i);
-            const uint32_t hhi = rdlane(rec[hi][kRHhi], i);
-            const uint32_t mi = rdlane(meta[hi], i);
+        for (int h = 0; h < SPL; ++h) {
+          key[h] = ((static_cast<uint64_t>(rec[h][kRHhi]) << 32) | rec[h][kRHlo]) ^
+                   (static_cast<uint64_t>(meta[h] + 1u) * 0xD6E8FEB86659FD93ull);
+          if (!alive0[h]) key[h] = ~0ull;
+          dup[h] = dup_by_sort(key[h], lane, slo[h], shi[h]) && alive0[h];
+        }
 #pragma unroll
-            for (int h = 0; h < SPL; ++h)
-              dup[h] = dup[h] || (j + 64 * h > i + 64 * hi && alive0[h] && rec[h][kRHlo] == hlo &&
-                                  rec[h][kRHhi] == hhi && meta[h] == mi);
+        for (int h = 1; h < SPL; ++h) {
+          // position of the first lower key >= key[h]
+          int pos = 0;
+          const uint64_t kh = key[h];
+#pragma unroll
+          for (int step = 32; step >= 1; step >>= 1) {
+            const int a = (pos + step - 1) << 2;
+            const uint64_t v = (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(a, static_cast<int>(shi[0])))) << 32) |
+                               static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(a, static_cast<int>(slo[0])));
+            pos += (v < kh) ? step : 0;
           }
+          // pos <= 63: the last lower key decides the 64th position
+          const uint64_t at = (static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(pos << 2, static_cast<int>(shi[0])))) << 32) |
+                              static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(pos << 2, static_cast<int>(slo[0])));
+          dup[h] = dup[h] || (alive0[h] && at == kh);
         }
       }
       if (p.flags & kFlagLogSumExp) {  // uniform
@@ -1811,14 +1891,25 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   if (tid == 0) p.status[b] = status;
 }
 
-template <int LPT, int NLEV, int SPL>
-hipError_t launch_nlev(const KernelParams& p, hipStream_t s) {
+template <int LPT, int NLEV, int SPL, bool SKIP>
+hipError_t launch_skip(const KernelParams& p, hipStream_t s) {
   dim3 grid(p.B), block(kThreads);
   if (p.bt_nodes != nullptr)
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP>), grid, block, 0, s, p);
   return hipGetLastError();
+}
+
+template <int LPT, int NLEV, int SPL>
+hipError_t launch_nlev(const KernelParams& p, hipStream_t s) {
+  // beams of more than one chunk (16 / LPT rows) skip ranks
+  if constexpr (SPL > 1) {
+    return launch_skip<LPT, NLEV, SPL, true>(p, s);
+  } else {
+    if (p.K > 16 / LPT) return launch_skip<LPT, NLEV, SPL, true>(p, s);
+    return launch_skip<LPT, NLEV, SPL, false>(p, s);
+  }
 }
 
 template <int LPT, int SPL>
