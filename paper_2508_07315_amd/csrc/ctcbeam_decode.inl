@@ -380,7 +380,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   __shared__ __align__(16) uint32_t s_row[(KMX + 16) * kRowWords];
   // beam state records by slot: [rcur] the current beam, [rcur ^ 1] its successors
   __shared__ __align__(16) uint32_t s_rec[2 * KMX * RW];
-  __shared__ float s_top[kWaves * 8 * SPL];
+  // group maxima of the bound; K <= 8: (row, wave) maxima, then wave maxima
+  __shared__ float s_top[kWaves * 8 * SPL + kWaves];
   __shared__ uint64_t s_red[2][kWaves];
   __shared__ int32_t s_nbuf, s_overflow;
   __shared__ int32_t s_best, s_bestlen;
@@ -831,6 +832,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       constexpr bool kKeepLm = HAS_LM && !HAS_BT;
       uint32_t lhi[kKeepLm ? NC : 1];
       float lmax = kNegInf;
+      float rmax[KCR];  // per chunk row: maximum over this lane's labels
 #pragma unroll
       for (int i = 0; i < KCR; ++i) {
 #pragma unroll
@@ -861,6 +863,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const float x = (c != klast[i]) ? x1 : x0;
           cand[r] = x;
           lmax = fmaxf(lmax, x);
+          rmax[i] = jj == 0 ? x : fmaxf(rmax[i], x);
         }
       }
       // LM entry (staged, or the token's unigram state) and boosting key of
@@ -910,9 +913,29 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         g = fmax_sel(g, xor_lane(g, 2, lane));
         if ((lane & 3) == 3) s_top[wave * 16 + (lane >> 2)] = g;
       } else if (K <= 8) {
+        // the 8 wave maxima, and the wave maxima of each of the first 8 rows:
+        // a transposed reduction halves the rows a lane carries at each of the
+        // lane-bit steps 1, 2, 4, leaving lane l with row 4(l&1) + 2(l>>1&1) +
+        // (l>>2&1), then reduces over lane bits 3..5
         const float g = row_max_last(lmax);
         const float g2 = fmax_sel(fmax_sel(rdlane(g, 15), rdlane(g, 31)), fmax_sel(rdlane(g, 47), rdlane(g, 63)));
-        if (lane == 0) s_top[wave] = g2;
+        if (lane == 0) s_top[kWaves * 8 + wave] = g2;
+        float m8[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) m8[i] = i < KCR ? rmax[i < KCR ? i : 0] : kNegInf;
+        const bool b0 = lane_in(0xAAAAAAAAAAAAAAAAull), b1 = lane_in(0xCCCCCCCCCCCCCCCCull), b2 = lane_in(kLanesBit2);
+        float m4[4], m2[2];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          m4[q] = fmaxf(b0 ? m8[q + 4] : m8[q], xor_lane(b0 ? m8[q] : m8[q + 4], 1, lane));
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+          m2[q] = fmaxf(b1 ? m4[q + 2] : m4[q], xor_lane(b1 ? m4[q] : m4[q + 2], 2, lane));
+        float m1 = fmaxf(b2 ? m2[1] : m2[0], xor_lane(b2 ? m2[0] : m2[1], 4, lane));
+        m1 = fmaxf(m1, xor_lane(m1, 8, lane));
+        m1 = fmaxf(m1, xor_lane(m1, 16, lane));
+        m1 = fmaxf(m1, xor_lane(m1, 32, lane));
+        if (lane < 8) s_top[wave * 8 + lane] = m1;
       } else if (K <= 32) {
         const float g = row_max_last(lmax);
         if ((lane & 15) == 15) s_top[wave * 4 + (lane >> 4)] = g;
@@ -926,8 +949,17 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       {
         float tc;
         if (K <= 8) {
-          const float v = wave_sort_desc<8>(lane < 8 ? s_top[lane] : kNegInf, lane);
-          tc = rdlane(v, K - 1);
+          // two bounds sorted side by side in groups of 16 lanes: lanes 0..15
+          // the maxima of (row, half of the waves), lanes 16..23 the wave
+          // maxima
+          float rw = s_top[lane];  // wave lane >> 3, row slot lane & 7
+          const float wm = s_top[kWaves * 8 + (lane & 7)];
+          rw = fmaxf(rw, xor_lane(rw, 8, lane));
+          rw = fmaxf(rw, xor_lane(rw, 16, lane));  // lanes 0..31: waves 0..3, lanes 32..63: 4..7
+          const float oh = xor_lane(rw, 32, lane);
+          float v = lane_in(0xFFull) ? rw : (lane_in(0xFF00ull) ? oh : (lane_in(0xFF0000ull) ? wm : kNegInf));
+          v = wave_sort_desc<16>(v, lane);
+          tc = fmaxf(rdlane(v, K - 1), rdlane(v, 16 + K - 1));
         } else if (K <= 32) {
           const float v = wave_sort_desc<32>(lane < 32 ? s_top[lane] : kNegInf, lane);
           tc = rdlane(v, K - 1);
@@ -1047,6 +1079,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             int myrank = K;
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
+              if (u > 0 && u * kWaves >= N) break;  // uniform: no entries left
               const int ql = wave + u * kWaves;
               const float xs = rdlane(xq, ql);
               const uint32_t is = rdlane(eq.y, ql);
