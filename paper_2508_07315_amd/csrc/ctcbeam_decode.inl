@@ -195,14 +195,6 @@ __device__ __forceinline__ float row_max_last(float v) {
   return v;
 }
 
-// maximum over each 8-lane group, valid in every lane of the group
-__device__ __forceinline__ float group8_max(float v, int lane) {
-  v = fmax_sel(v, xor_lane(v, 1, lane));
-  v = fmax_sel(v, xor_lane(v, 2, lane));
-  v = fmax_sel(v, xor_lane(v, 4, lane));
-  return v;
-}
-
 // lanes that keep the larger value in the bitonic step (k, j) of a sort of
 // groups of N lanes, descending
 constexpr uint64_t bitonic_max_lanes(int k, int j, int N) {
@@ -361,6 +353,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr int NC = KCR * LPT;               // candidates per lane
   // a chunk has at most 64 LM segments (beam, level): one lane each
   constexpr int KSEG = (NL > 0 && KCR * NL > 64) ? 64 / (NL > 0 ? NL : 1) : KCR;
+  // without rank skipping the beam fits one chunk of 16 / LPT rows: K <= 8
+  // for two or more labels per lane
+  constexpr bool kSmallK = SPL == 1 && !SKIP && LPT >= 2;
   constexpr int kRowWords = 16;               // beam record per live position
   // beam state record (one per slot, double-buffered by frame): score bits,
   // back-pointer, transcript hash (2), length, last label, LM state, boosting
@@ -620,6 +615,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       if (lane < K) rBlankN = __builtin_nontemporal_load(rowp + V);
     }
     float tau_run = kNegInf;
+    float gacc = kNegInf;  // top 64 group maxima of the frame's chunks so far (K > 8)
     int nfin = 0;
     // survivors carried in the pool from chunks whose rank was skipped
     int carry = 0;
@@ -904,25 +900,33 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         s_nbuf = 0;  // the previous rank read it before barrier D
         s_overflow = 0;
       }
-      // Maxima of disjoint lane groups are distinct candidates, so the K-th
-      // largest of at least K group maxima bounds the K-th best candidate
-      // from below.  K <= 8: the 8 wave maxima; K <= 32: the 32 rows of 16
-      // lanes; K <= 64: 64 groups of 8 lanes; otherwise 128 groups of 4.
+      // Maxima of disjoint candidate groups are distinct candidates, so the
+      // K-th largest of at least K group maxima bounds the K-th best candidate
+      // from below.  One slot per lane: groups (row, wave) of this chunk, and
+      // for K <= 8 also (row, half of the waves) and the waves; the groups of
+      // earlier chunks of the frame still count.  Two slots per lane: 128
+      // groups of 4 lanes.
       if (SPL > 1) {
         float g = fmax_sel(lmax, xor_lane(lmax, 1, lane));
         g = fmax_sel(g, xor_lane(g, 2, lane));
         if ((lane & 3) == 3) s_top[wave * 16 + (lane >> 2)] = g;
-      } else if (K <= 8) {
-        // the 8 wave maxima, and the wave maxima of each of the first 8 rows:
-        // a transposed reduction halves the rows a lane carries at each of the
-        // lane-bit steps 1, 2, 4, leaving lane l with row 4(l&1) + 2(l>>1&1) +
-        // (l>>2&1), then reduces over lane bits 3..5
-        const float g = row_max_last(lmax);
-        const float g2 = fmax_sel(fmax_sel(rdlane(g, 15), rdlane(g, 31)), fmax_sel(rdlane(g, 47), rdlane(g, 63)));
-        if (lane == 0) s_top[kWaves * 8 + wave] = g2;
+      } else {
+        // The wave maxima of 8 row groups (row i, and i + 8 when a chunk has
+        // 16 rows): a transposed reduction halves the groups a lane carries
+        // at each of the lane-bit steps 1, 2, 4, leaving lane l with group
+        // 4(l&1) + 2(l>>1&1) + (l>>2&1), then reduces over lane bits 3..5.
+        // K <= 8 also keeps the 8 wave maxima.
+        if (kSmallK || K <= 8) {
+          const float g = row_max_last(lmax);
+          const float g2 = fmax_sel(fmax_sel(rdlane(g, 15), rdlane(g, 31)), fmax_sel(rdlane(g, 47), rdlane(g, 63)));
+          if (lane == 0) s_top[kWaves * 8 + wave] = g2;
+        }
         float m8[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) m8[i] = i < KCR ? rmax[i < KCR ? i : 0] : kNegInf;
+        for (int i = 0; i < 8; ++i) {
+          m8[i] = i < KCR ? rmax[i < KCR ? i : 0] : kNegInf;
+          if (i + 8 < KCR) m8[i] = fmaxf(m8[i], rmax[i + 8 < KCR ? i + 8 : 0]);
+        }
         const bool b0 = lane_in(0xAAAAAAAAAAAAAAAAull), b1 = lane_in(0xCCCCCCCCCCCCCCCCull), b2 = lane_in(kLanesBit2);
         float m4[4], m2[2];
 #pragma unroll
@@ -936,19 +940,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         m1 = fmaxf(m1, xor_lane(m1, 16, lane));
         m1 = fmaxf(m1, xor_lane(m1, 32, lane));
         if (lane < 8) s_top[wave * 8 + lane] = m1;
-      } else if (K <= 32) {
-        const float g = row_max_last(lmax);
-        if ((lane & 15) == 15) s_top[wave * 4 + (lane >> 4)] = g;
-      } else {
-        const float g = group8_max(lmax, lane);
-        if ((lane & 7) == 7) s_top[wave * 8 + (lane >> 3)] = g;
       }
       __syncthreads();  // B: bound inputs, blanks, pool reset
 
       // ---- T. bound and filter ----
       {
         float tc;
-        if (K <= 8) {
+        if (kSmallK || K <= 8) {
           // two bounds sorted side by side in groups of 16 lanes: lanes 0..15
           // the maxima of (row, half of the waves), lanes 16..23 the wave
           // maxima
@@ -960,12 +958,14 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           float v = lane_in(0xFFull) ? rw : (lane_in(0xFF00ull) ? oh : (lane_in(0xFF0000ull) ? wm : kNegInf));
           v = wave_sort_desc<16>(v, lane);
           tc = fmaxf(rdlane(v, K - 1), rdlane(v, 16 + K - 1));
-        } else if (K <= 32) {
-          const float v = wave_sort_desc<32>(lane < 32 ? s_top[lane] : kNegInf, lane);
-          tc = rdlane(v, K - 1);
         } else if (SPL == 1) {
-          const float v = wave_sort_desc<64>(s_top[lane], lane);
-          tc = rdlane(v, K - 1);
+          // this chunk's 64 (row group, wave) maxima, sorted ascending, merged
+          // into the frame's running top 64 (descending): the elementwise
+          // maximum of the two is bitonic and holds the top 64 of the union
+          // (without rank skipping each chunk's rank sets tau_run instead)
+          const float v = -wave_sort_desc<64>(-s_top[lane], lane);
+          gacc = bitonic_merge<64, 64, 32>(fmaxf(SKIP ? gacc : kNegInf, v), lane);
+          tc = rdlane(gacc, K - 1);
         } else {
           // K-th largest of 128 maxima, two sorted halves a and b: the largest
           // value x with at least K maxima >= x (counts by binary search)
