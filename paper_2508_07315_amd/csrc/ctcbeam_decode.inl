@@ -1004,14 +1004,16 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         if (K > 16) tb = fmin_sel(tb, xor_lane(tb, 16, lane));
         if (K > 32) tb = fmin_sel(tb, xor_lane(tb, 32, lane));
         const float tblank = rdlane(tb, 0);
-        const float tau = fmaxf(fmaxf(tau_run, tc), tblank);
-        uint32_t qmask = 0u;
+        // an infinite bound admits every finite candidate and no -inf one
+        const float tau = fmaxf(fmaxf(fmaxf(tau_run, tc), tblank), -__FLT_MAX__);
+        // most waves hold no survivor: their lane maxima say so
+        if (__ballot(lmax >= tau) != 0ull) {  // uniform
+          uint32_t qmask = 0u;
 #pragma unroll
-        for (int r = 0; r < NC; ++r) qmask |= (cand[r] >= tau && cand[r] != kNegInf) ? (1u << r) : 0u;
-        const int mycnt = __popc(qmask);
-        const int incl = wave_incl_scan(mycnt, lane);
-        const int wtotal = rdlane(incl, 63);
-        if (wtotal > 0) {
+          for (int r = 0; r < NC; ++r) qmask |= (cand[r] >= tau) ? (1u << r) : 0u;
+          const int mycnt = __popc(qmask);
+          const int incl = wave_incl_scan(mycnt, lane);
+          const int wtotal = rdlane(incl, 63);
           int wbase = 0;
           if (lane == 0) wbase = atomicAdd(&s_nbuf, wtotal);
           wbase = __builtin_amdgcn_readfirstlane(wbase);
