@@ -166,6 +166,15 @@ int ctcbeam_decode(const float* logprobs, const int32_t* lengths, int B, int T, 
 #define CTCBEAM_FLAG_BOOST_ROLLBACK 2  /* after LM.Final, live hypotheses get
                                           fl(boost_w * -pending), taking back the
                                           boosting of an unfinished phrase */
+#define CTCBEAM_FLAG_NO_ROW_CACHE 4    /* performance only, identical results:
+                                          refill the per-token LM rows of every
+                                          beam every frame instead of keeping
+                                          one row per LM state across frames
+                                          (rows are reused with an LM of at
+                                          most 2^23 states, no boosting, and
+                                          V of 513..1024 with K <= 8, up to
+                                          2048 with K <= 4, up to 4096 with
+                                          K <= 2) */
 
 typedef struct ctcbeam_opts {
   float prune_theta;   /* Algorithm 1 threshold theta; +inf disables pruning */

@@ -106,12 +106,14 @@ class _Opts(ctypes.Structure):
 
 FLAG_LOGSUMEXP = 1        # CTCBEAM_FLAG_LOGSUMEXP
 FLAG_BOOST_ROLLBACK = 2   # CTCBEAM_FLAG_BOOST_ROLLBACK
+FLAG_NO_ROW_CACHE = 4     # CTCBEAM_FLAG_NO_ROW_CACHE
 
 
-def _opts(theta, stats, B, logsumexp, boost_rollback):
+def _opts(theta, stats, B, logsumexp, boost_rollback, row_cache=True):
     """ctcbeam_opts by reference, or None when every option is at its default."""
     import torch
-    flags = (FLAG_LOGSUMEXP if logsumexp else 0) | (FLAG_BOOST_ROLLBACK if boost_rollback else 0)
+    flags = (FLAG_LOGSUMEXP if logsumexp else 0) | (FLAG_BOOST_ROLLBACK if boost_rollback else 0) | \
+        (0 if row_cache else FLAG_NO_ROW_CACHE)
     if (theta is None or math.isinf(theta)) and stats is None and flags == 0:
         return None
     o = _Opts()
@@ -296,12 +298,13 @@ def ctcbeam_decode_ex(logprobs, lengths, K: int, alpha: float = 0.0, beta: float
                       boost: Optional[Boost] = None, workspace=None, out_tokens=None,
                       out_lengths=None, out_scores=None, stream=None,
                       theta: float = math.inf, stats=None, logsumexp: bool = False,
-                      boost_rollback: bool = False):
+                      boost_rollback: bool = False, row_cache: bool = True):
     """Enqueue one decode on ``stream`` (default: torch's current stream).
 
     logprobs: float32 [B, T, V+1] device tensor (blank = V); lengths: int32 [B].
-    Outputs are allocated when not given.  Returns (tokens [B,T] int32 with -1
-    padding, lengths [B] int32, scores [B] float32, workspace uint8)."""
+    Outputs are allocated when not given.  ``row_cache=False`` sets
+    CTCBEAM_FLAG_NO_ROW_CACHE (same results).  Returns (tokens [B,T] int32
+    with -1 padding, lengths [B] int32, scores [B] float32, workspace uint8)."""
     import torch
     lib = _load()
     if logprobs.dim() != 3:
@@ -319,7 +322,7 @@ def ctcbeam_decode_ex(logprobs, lengths, K: int, alpha: float = 0.0, beta: float
     if workspace is None:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
     ws = _dptr(workspace, torch.uint8, "workspace")
-    o = _opts(theta, stats, B, logsumexp, boost_rollback)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache)
     opts = None if o is None else ctypes.byref(o)
     if stream is None:
         stream = torch.cuda.current_stream(dev).cuda_stream
@@ -348,7 +351,7 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
                          boost: Optional[Boost] = None, workspace=None, nbest_tokens=None,
                          nbest_lengths=None, nbest_scores=None, stream=None,
                          theta: float = math.inf, stats=None, logsumexp: bool = False,
-                         boost_rollback: bool = False):
+                         boost_rollback: bool = False, row_cache: bool = True):
     """Enqueue one N-best decode on ``stream`` (default: torch's current stream).
 
     Same inputs as ``ctcbeam_decode_ex``.  Returns (tokens [B,K,T] int32 with
@@ -372,7 +375,7 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
     if workspace is None:
         workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
     ws = _dptr(workspace, torch.uint8, "workspace")
-    o = _opts(theta, stats, B, logsumexp, boost_rollback)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache)
     opts = None if o is None else ctypes.byref(o)
     if stream is None:
         stream = torch.cuda.current_stream(dev).cuda_stream

@@ -68,6 +68,8 @@ constexpr int kGenShift = 26;
 constexpr uint32_t kGenMax = 63u;
 constexpr uint32_t kLowMask = (1u << kGenShift) - 1u;
 constexpr int kTileUnroll = 8;
+// LM target state in a cached row entry (the states are numbered below 2^23)
+constexpr uint32_t kTargetMask = (1u << 23) - 1u;
 
 __device__ __forceinline__ uint64_t mix_token(uint64_t h, uint32_t c) {
   uint64_t z = h + (static_cast<uint64_t>(c) + 1ull) * 0x9E3779B97F4A7C15ull;
@@ -334,7 +336,10 @@ __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
 // j / 64 (SPL = 2 serves beams of 65..128).  SKIP: ranks of chunks before
 // the last are skipped while the survivor pool has room (beams above one
 // chunk; small beams keep one rank per chunk and the simpler code).
-template <int LPT, int NLEV, bool HAS_BT, int SPL, bool SKIP>
+// CACHE (one chunk, one slot per lane, LM without boosting, LM states below
+// 2^23): LM key rows are kept per LM state across frames and only the states
+// new to the rows are filled; an entry holds its arc's target state.
+template <int LPT, int NLEV, bool HAS_BT, int SPL, bool SKIP, bool CACHE>
 __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool HAS_LM = NLEV >= 0;
   constexpr int NL = NLEV > 0 ? NLEV : 0;     // chain levels above the unigram root
@@ -356,6 +361,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // without rank skipping the beam fits one chunk of 16 / LPT rows: K <= 8
   // for two or more labels per lane
   constexpr bool kSmallK = SPL == 1 && !SKIP && LPT >= 2;
+  static_assert(!CACHE || (kSmallK && HAS_LM && NL > 0 && !HAS_BT), "row caching needs one chunk and an LM");
   constexpr int kRowWords = 16;               // beam record per live position
   // beam state record (one per slot, double-buffered by frame): score bits,
   // back-pointer, transcript hash (2), length, last label, LM state, boosting
@@ -466,12 +472,27 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       btpot[0] = static_cast<int32_t>(nd.pot & 0xFFu);
     }
   }
+  // Row cache (CACHE): lane r < KCR holds the LM state of key row r and the
+  // generation it was filled with; lane j the row of slot j, that row's
+  // generation, and whether slot j fills it in the next frame.
+  uint32_t rtag = 0xFFFFFFFFu, rgen = 0u, rgj = 0u;
+  int rowof = 0;
+  bool fillrep = false;
+  if (CACHE && j == 0 && L > 0) {
+    rtag = p.lm_bos_state;
+    rgen = 1u;  // the first fill's generation
+    rgj = 1u;
+    fillrep = true;
+  }
   // beam record of live position lp for slot j + 64 h (written by wave 0 for
-  // the live slots)
+  // the live slots); with CACHE the slot field also carries the key row
+  // (bits 8..15) and its generation (bits 16..21)
   auto put_row = [&](int lp, int h) __attribute__((always_inline)) {
     uint32_t* rr = s_row + lp * kRowWords;
+    const uint32_t zf = static_cast<uint32_t>(j + 64 * h) |
+                        (CACHE ? (static_cast<uint32_t>(rowof) << 8) | (rgj << 16) : 0u);
     *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc[h]), static_cast<uint32_t>(last[h]),
-                                               static_cast<uint32_t>(j + 64 * h), static_cast<uint32_t>(btpot[h]));
+                                               zf, static_cast<uint32_t>(btpot[h]));
 #pragma unroll
     for (int l0 = 0; l0 < NL; l0 += 4) {
       const auto bo_at = [&](int l) __attribute__((always_inline)) { return l < NL ? __float_as_uint(lvbo[h][l < NLA ? l : 0]) : 0u; };
@@ -665,7 +686,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         for (int l = 0; l < NL; ++l) {
 #pragma unroll
           for (int h = 0; h < SPL; ++h) {
-            const uint32_t n = inch[h] ? (lvc[h][l] & ~kExists) : 0u;
+            const uint32_t n = (CACHE ? fillrep : inch[h]) ? (lvc[h][l] & ~kExists) : 0u;
             const uint64_t m = __ballot(n != 0u);
             const int nl = __popcll(m);
             if (nl > 0) {  // wave-uniform
@@ -677,7 +698,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               const uint32_t r_base =
                   static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(lvb[h][l])));
               const uint32_t r_rl =
-                  static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, row[h] | (l << 8)));
+                  static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, (CACHE ? rowof : row[h]) | (l << 8)));
               float r_f[NF];
 #pragma unroll
               for (int k = 0; k + 1 < NL; ++k) {
@@ -734,8 +755,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 #pragma unroll
               for (int k = 0; k + 1 < NL; ++k) v = v + af[u][k];
               const float av = alpha * v;
-              tgt[q] = a[u].target;
-              const uint32_t hi = genhi | (((arl[u] >> 8) + 1u) << 23) | q;
+              uint32_t hi = genhi | (((arl[u] >> 8) + 1u) << 23);
+              if constexpr (CACHE) {
+                hi |= a[u].target;  // below 2^23
+              } else {
+                tgt[q] = a[u].target;
+                hi |= q;
+              }
               atomicMax(reinterpret_cast<unsigned long long*>(&lmrow[(arl[u] & 0xFFu) * V + a[u].token]),
                         (static_cast<unsigned long long>(hi) << 32) | __float_as_uint(av));
             }
@@ -805,13 +831,17 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       int klast[KCR];
       float kbo[KCR][NLA];
       int kpot[KCR];
+      // LM key row of chunk row i and the generation its entries carry
+      uint32_t krow[KCR], kgenhi[KCR];
 #pragma unroll
       for (int i = 0; i < KCR; ++i) {
         const uint32_t* rr = s_row + (cs + i) * kRowWords;
         const uint4 h0 = *reinterpret_cast<const uint4*>(rr);
         ksc[i] = (i < kc) ? __uint_as_float(h0.x) : kNegInf;
         klast[i] = static_cast<int>(h0.y);
-        kslot[i] = static_cast<int>(h0.z);
+        kslot[i] = static_cast<int>(CACHE ? (h0.z & 0xFFu) : h0.z);
+        krow[i] = CACHE ? ((h0.z >> 8) & 0xFFu) : static_cast<uint32_t>(i);
+        kgenhi[i] = CACHE ? ((h0.z >> 16) << kGenShift) : genhi;
         kpot[i] = static_cast<int>(h0.w);
 #pragma unroll
         for (int l0 = 0; l0 < NL; l0 += 4) {
@@ -839,15 +869,17 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const float x0 = ksc[i] + rD[jj];
           float x1 = x0 + beta;
           if (HAS_LM) {
-            const uint64_t ent = lmrow[e];
+            const uint64_t ent = lmrow[CACHE ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e];
             const uint32_t hi = static_cast<uint32_t>(ent >> 32);
             float v = rP1[jj];
 #pragma unroll
             for (int l = 0; l < NL; ++l) v = v + kbo[i][l];
-            const bool has = hi >= genhi;
+            const bool has = hi >= kgenhi[i];
             const float av = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
             x1 = x1 + av;
-            if constexpr (kKeepLm) lhi[r] = has ? hi : rcc[jj];
+            // the LM target: with CACHE the entry's own, else its staging
+            // slot (resolved later), or the token's unigram state
+            if constexpr (kKeepLm) lhi[r] = has ? (CACHE ? (hi & kTargetMask) : hi) : rcc[jj];
           }
           if (HAS_BT) {
             const uint32_t be = btrow[e];
@@ -870,8 +902,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         lraw = 0u;
         bk = 0u;
         if (HAS_LM) {
-          const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
-          lraw = hi >= genhi ? hi : rcc[jj];
+          const uint32_t hi = static_cast<uint32_t>(lmrow[CACHE ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e] >> 32);
+          lraw = hi >= kgenhi[i] ? (CACHE ? (hi & kTargetMask) : hi) : rcc[jj];
         }
         if (HAS_BT) {
           const uint32_t be = btrow[e];
@@ -1075,7 +1107,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             nfin = __popcll(__ballot(xq != kNegInf));
             const bool own = ((lane & (kWaves - 1)) == wave) && xq != kNegInf;
             uint32_t lmt = eq.z;
-            if (HAS_LM && !SKIP && lane >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+            if (HAS_LM && !SKIP && !CACHE && lane >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
             Succ sp;
             if (last_chunk) succ_begin(own, eq.y, lmt, eq.w, prec, sp);  // loads overlap the ranking
             int myrank = K;
@@ -1132,7 +1164,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               for (int u = 0; u < 8; ++u) myrank = ((lane >> 3) == u) ? rk[u] : myrank;
               const bool win = (lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf;
               uint32_t lmt = eq.z;
-              if (HAS_LM && !SKIP && win && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+              if (HAS_LM && !SKIP && !CACHE && win && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
               if (last_chunk) {
                 Succ sp;
                 succ_begin(win, eq.y, lmt, eq.w, prec, sp);
@@ -1154,7 +1186,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             // the best register candidate's fields, tracked by selects so that
             // no candidate array is indexed at run time
             float wx = kNegInf;
-            uint32_t wflat = 0u, wi = 0u, wjj = 0u;
+            uint32_t wflat = 0u, wi = 0u, wjj = 0u, wrow = 0u, wgen = 0u;
 #pragma unroll
             for (int r = 0; r < NC; ++r) {
               if (cand[r] != kNegInf) {
@@ -1169,6 +1201,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   wflat = flat;
                   wi = static_cast<uint32_t>(i);
                   wjj = static_cast<uint32_t>(jj);
+                  if constexpr (CACHE) {
+                    wrow = krow[i];
+                    wgen = kgenhi[i];
+                  }
                 }
               }
             }
@@ -1212,8 +1248,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                 const uint32_t e = wi * static_cast<uint32_t>(V) + c;
                 uint32_t lmt = 0u, bk = 0u;
                 if (HAS_LM) {
-                  const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
-                  lmt = hi >= genhi ? tgt[hi & 0xFFFu] : c;
+                  if constexpr (CACHE) {
+                    const uint32_t hi = static_cast<uint32_t>(lmrow[wrow * static_cast<uint32_t>(V) + c] >> 32);
+                    lmt = hi >= wgen ? (hi & kTargetMask) : c;
+                  } else {
+                    const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
+                    lmt = hi >= genhi ? tgt[hi & 0xFFFu] : c;
+                  }
                 }
                 if (HAS_BT) {
                   const uint32_t be = btrow[e];
@@ -1367,12 +1408,53 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       const uint64_t amask = __ballot(nalive);
       const int na = __popcll(amask);
       const int lp = __popcll(amask & lmlt);
+      if constexpr (CACHE) {
+        // Key rows of the new beam: a live slot whose LM state has a row
+        // keeps it; each other state takes a row no live slot uses (there are
+        // K <= KCR rows) and its first slot fills it in the next frame.  When
+        // the next fill wraps the generation every row is cleared, so every
+        // state is new.
+        const uint32_t st = rec[kRLms];
+        const bool wrap = gen == kGenMax;
+        const uint32_t ngen = wrap ? 1u : gen + 1u;
+        if (wrap) rtag = 0xFFFFFFFFu;
+        uint32_t used = 0u;
+        bool hit = false;
+#pragma unroll
+        for (int r = 0; r < KCR; ++r) {
+          const uint32_t tr = rdlane(rtag, r);
+          const bool h = nalive && st == tr;
+          if (__ballot(h) != 0ull) used |= 1u << r;
+          rowof = h ? r : rowof;
+          rgj = h ? rdlane(rgen, r) : rgj;
+          hit = hit || h;
+        }
+        bool miss = nalive && !hit;
+        fillrep = false;
+        uint64_t mm = __ballot(miss);
+        while (mm != 0ull) {  // uniform
+          const int jm = static_cast<int>(__builtin_ctzll(mm));
+          const uint32_t sj = rdlane(st, jm);
+          const bool same = miss && st == sj;
+          const int r = min(__builtin_ctz(~used), KCR - 1);  // a free row: < KCR
+          used |= 1u << r;
+          if (lane == r) {
+            rtag = sj;
+            rgen = ngen;
+          }
+          rowof = same ? r : rowof;
+          rgj = same ? ngen : rgj;
+          fillrep = fillrep || j == jm;
+          miss = miss && !same;
+          mm = __ballot(miss);
+        }
+      }
       if (wave == 0 && nalive) put_row(lp, 0);
       // chunk plan: live slots in slot order, at most kcmax beams and
-      // kLmStage staged arcs per chunk
+      // kLmStage staged arcs per chunk (cached rows stage nothing)
       const int ia = wave_incl_scan(acnt, lane);
       const int tota = rdlane(ia, 63);
-      if (na <= kcmax && tota <= kLmStage) {
+      if (na <= kcmax && (CACHE || tota <= kLmStage)) {
         nch = na > 0 ? 1 : 0;
         cid[0] = 0;
       } else {
@@ -1929,10 +2011,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 template <int LPT, int NLEV, int SPL, bool SKIP>
 hipError_t launch_skip(const KernelParams& p, hipStream_t s) {
   dim3 grid(p.B), block(kThreads);
+  constexpr bool kCacheable = SPL == 1 && !SKIP && LPT >= 2 && NLEV > 0;
   if (p.bt_nodes != nullptr)
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP, false>), grid, block, 0, s, p);
+  else if (kCacheable && p.lm_states_below_2p23 && !(p.flags & kFlagNoRowCache))
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, kCacheable>), grid, block, 0, s, p);
   else
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, false>), grid, block, 0, s, p);
   return hipGetLastError();
 }
 

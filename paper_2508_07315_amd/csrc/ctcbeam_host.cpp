@@ -798,6 +798,7 @@ size_t ctcbeam_workspace_bytes(int B, int T, int K) {
 static_assert(CTCBEAM_MAX_K == ctcbeam::kMaxK, "beam size limit");
 static_assert(CTCBEAM_FLAG_LOGSUMEXP == ctcbeam::kFlagLogSumExp, "flag values");
 static_assert(CTCBEAM_FLAG_BOOST_ROLLBACK == ctcbeam::kFlagBoostRollback, "flag values");
+static_assert(CTCBEAM_FLAG_NO_ROW_CACHE == ctcbeam::kFlagNoRowCache, "flag values");
 
 namespace {
 
@@ -825,7 +826,8 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
   if (std::isnan(theta) || theta < 0.0f) return fail(1, "prune_theta must be >= 0 (or +inf)");
   if (std::isnan(alpha) || std::isnan(beta) || std::isnan(boost_w)) return fail(1, "NaN weight");
   const int flags = opts ? opts->flags : 0;
-  if (flags & ~(CTCBEAM_FLAG_LOGSUMEXP | CTCBEAM_FLAG_BOOST_ROLLBACK)) return fail(1, "unknown flag bits");
+  if (flags & ~(CTCBEAM_FLAG_LOGSUMEXP | CTCBEAM_FLAG_BOOST_ROLLBACK | CTCBEAM_FLAG_NO_ROW_CACHE))
+    return fail(1, "unknown flag bits");
   if (B == 0) return 0;
   if (!lengths || !workspace || (T > 0 && !logprobs)) return fail(1, "null device pointer");
   if (want_nbest ? (!nbest_lengths || !nbest_scores || (T > 0 && !nbest_tokens))
@@ -853,6 +855,7 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
     p.lm_arcs = lm->d_arcs;
     p.lm_unigram = lm->d_unigram;
     p.lm_nlev = lm->nlev;
+    p.lm_states_below_2p23 = lm->n_states <= (int64_t(1) << 23) ? 1 : 0;
     p.lm_bos_state = static_cast<uint32_t>(V);
   }
   if (boost) {

@@ -15,6 +15,7 @@ constexpr int kCap = 512;             // survivor pool entries
 constexpr uint32_t kExists = 0x80000000u;
 constexpr int kFlagLogSumExp = 1;      // recombination by log-sum-exp
 constexpr int kFlagBoostRollback = 2;  // pending boosting taken back at the end
+constexpr int kFlagNoRowCache = 4;     // LM key rows refilled for every beam every frame
 
 // LM state record, one per chain level l (context of length l+1):
 //   {arc_begin, arc_count | kExists, backoff bits}
@@ -54,6 +55,7 @@ struct KernelParams {
   const float* lm_unigram;   // [V+1], index V = </s>
   int lm_nlev;
   uint32_t lm_bos_state;
+  int lm_states_below_2p23;  // every LM state id fits 23 bits
   // boosting (null when disabled)
   const BtNode* bt_nodes;
   const BtEntry* bt_list;

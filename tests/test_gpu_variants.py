@@ -161,7 +161,7 @@ def test_unknown_flag_bits_are_rejected():
     sc = torch.empty((1,), dtype=torch.float32, device=device())
     o = P._Opts()
     o.prune_theta = math.inf
-    o.flags = 4
+    o.flags = 8
     rc = lib.ctcbeam_decode_ex(ctypes.c_void_p(d_lp.data_ptr()), ctypes.c_void_p(d_len.data_ptr()),
                                1, 3, 4, 2, 0.0, 0.0, 0.0, None, None, ctypes.c_void_p(ws.data_ptr()),
                                ws.numel(), ctypes.c_void_p(tok.data_ptr()), None,
