@@ -141,6 +141,12 @@ constexpr int kDppRowShr2 = 0x112;
 constexpr int kDppRowShr4 = 0x114;
 constexpr int kDppRowShr8 = 0x118;
 constexpr int kDppRowRor8 = 0x128;
+// rotation by D within each 16-lane row (D = 0: the value itself)
+template <int D>
+__device__ __forceinline__ uint32_t dpp_row_ror(uint32_t v) {
+  if constexpr (D == 0) return v;
+  else return dpp_full<0x120 + D>(v);
+}
 
 // value of lane (lane ^ j); j must be a compile-time power of two <= 32 after
 // unrolling
@@ -1414,21 +1420,44 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         // K <= KCR rows) and its first slot fills it in the next frame.  When
         // the next fill wraps the generation every row is cleared, so every
         // state is new.
+        // The slots (lanes 0..K-1) meet the row tags (lanes 0..7, rows past
+        // KCR empty) through rotations within 16 lanes, lanes 8..15 holding
+        // a copy of lanes 0..7.
         const uint32_t st = rec[kRLms];
         const bool wrap = gen == kGenMax;
         const uint32_t ngen = wrap ? 1u : gen + 1u;
         if (wrap) rtag = 0xFFFFFFFFu;
-        uint32_t used = 0u;
+        const bool hi8 = lane_in_here<0xFF00FF00FF00FF00ull>();
+        const uint32_t rt8 = hi8 ? dpp_row_ror<8>(rtag) : rtag;
+        const uint32_t rg8 = hi8 ? dpp_row_ror<8>(rgen) : rgen;
+        const uint32_t ri8 = static_cast<uint32_t>(lane & 7);
         bool hit = false;
-#pragma unroll
-        for (int r = 0; r < KCR; ++r) {
-          const uint32_t tr = rdlane(rtag, r);
-          const bool h = nalive && st == tr;
-          if (__ballot(h) != 0ull) used |= 1u << r;
-          rowof = h ? r : rowof;
-          rgj = h ? rdlane(rgen, r) : rgj;
+        uint32_t hrow = 0u, hgen = 0u;
+        const auto probe = [&](uint32_t td, uint32_t gd, uint32_t id) __attribute__((always_inline)) {
+          const bool h = st == td;
+          hrow = h ? id : hrow;
+          hgen = h ? gd : hgen;
           hit = hit || h;
+        };
+        probe(rt8, rg8, ri8);
+        probe(dpp_row_ror<1>(rt8), dpp_row_ror<1>(rg8), dpp_row_ror<1>(ri8));
+        probe(dpp_row_ror<2>(rt8), dpp_row_ror<2>(rg8), dpp_row_ror<2>(ri8));
+        probe(dpp_row_ror<3>(rt8), dpp_row_ror<3>(rg8), dpp_row_ror<3>(ri8));
+        probe(dpp_row_ror<4>(rt8), dpp_row_ror<4>(rg8), dpp_row_ror<4>(ri8));
+        probe(dpp_row_ror<5>(rt8), dpp_row_ror<5>(rg8), dpp_row_ror<5>(ri8));
+        probe(dpp_row_ror<6>(rt8), dpp_row_ror<6>(rg8), dpp_row_ror<6>(ri8));
+        probe(dpp_row_ror<7>(rt8), dpp_row_ror<7>(rg8), dpp_row_ror<7>(ri8));
+        hit = hit && nalive;
+        if (hit) {
+          rowof = static_cast<int>(hrow);
+          rgj = hgen;
         }
+        // rows used by a live slot (slots are lanes 0..7)
+        uint32_t ub = hit ? (1u << hrow) : 0u;
+        ub |= xor_lane(ub, 1, lane);
+        ub |= xor_lane(ub, 2, lane);
+        ub |= xor_lane(ub, 4, lane);
+        uint32_t used = rdlane(ub, 0);
         bool miss = nalive && !hit;
         fillrep = false;
         uint64_t mm = __ballot(miss);
