@@ -478,25 +478,22 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       btpot[0] = static_cast<int32_t>(nd.pot & 0xFFu);
     }
   }
-  // Row cache (CACHE): lane r < KCR holds the LM state of key row r and the
-  // generation it was filled with; lane j the row of slot j, that row's
-  // generation, and whether slot j fills it in the next frame.
-  uint32_t rtag = 0xFFFFFFFFu, rgen = 0u, rgj = 0u;
+  // Row cache (CACHE): lane r < KCR holds the LM state of key row r; lane j
+  // the row of slot j and whether slot j fills it in the next frame.  A
+  // filled row holds an entry for every token.
+  uint32_t rtag = 0xFFFFFFFFu;
   int rowof = 0;
   bool fillrep = false;
   if (CACHE && j == 0 && L > 0) {
     rtag = p.lm_bos_state;
-    rgen = 1u;  // the first fill's generation
-    rgj = 1u;
     fillrep = true;
   }
   // beam record of live position lp for slot j + 64 h (written by wave 0 for
   // the live slots); with CACHE the slot field also carries the key row
-  // (bits 8..15) and its generation (bits 16..21)
+  // (bits 8..15)
   auto put_row = [&](int lp, int h) __attribute__((always_inline)) {
     uint32_t* rr = s_row + lp * kRowWords;
-    const uint32_t zf = static_cast<uint32_t>(j + 64 * h) |
-                        (CACHE ? (static_cast<uint32_t>(rowof) << 8) | (rgj << 16) : 0u);
+    const uint32_t zf = static_cast<uint32_t>(j + 64 * h) | (CACHE ? static_cast<uint32_t>(rowof) << 8 : 0u);
     *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc[h]), static_cast<uint32_t>(last[h]),
                                                zf, static_cast<uint32_t>(btpot[h]));
 #pragma unroll
@@ -723,6 +720,31 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
           }
         }
+        if constexpr (CACHE) {
+          // every token of a new row gets its unigram + backoff fold as an
+          // order-0 entry (the explicit arcs, order >= 1, win the maximum),
+          // so the scoring reads one entry per token and nothing else
+          uint64_t fm = __ballot(fillrep);
+          while (fm != 0ull) {  // uniform
+            const int jr = static_cast<int>(__builtin_ctzll(fm));
+            fm &= fm - 1ull;
+            const uint32_t rf = rdlane(static_cast<uint32_t>(rowof), jr);
+            float bo[NLA];
+#pragma unroll
+            for (int l = 0; l < NL; ++l) bo[l] = rdlane(lvbo[0][l], jr);
+#pragma unroll
+            for (int jj = 0; jj < LPT; ++jj) {
+              if (tid + jj * kThreads < V) {
+                float v = rP1[jj];
+#pragma unroll
+                for (int l = 0; l < NL; ++l) v = v + bo[l];
+                const float av = alpha * v;
+                atomicMax(reinterpret_cast<unsigned long long*>(&lmrow[rf * static_cast<uint32_t>(V) + rcc[jj]]),
+                          (static_cast<unsigned long long>(genhi | rcc[jj]) << 32) | __float_as_uint(av));
+              }
+            }
+          }
+        }
         // tiles of 64 arcs never straddle segments: a tile's segment is one
         // ballot away and its fields are wave-uniform (readlane)
         const int sincl = wave_incl_scan(static_cast<int>(sg_cnt), lane);
@@ -837,8 +859,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       int klast[KCR];
       float kbo[KCR][NLA];
       int kpot[KCR];
-      // LM key row of chunk row i and the generation its entries carry
-      uint32_t krow[KCR], kgenhi[KCR];
+      // LM key row of chunk row i
+      uint32_t krow[KCR];
 #pragma unroll
       for (int i = 0; i < KCR; ++i) {
         const uint32_t* rr = s_row + (cs + i) * kRowWords;
@@ -847,10 +869,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         klast[i] = static_cast<int>(h0.y);
         kslot[i] = static_cast<int>(CACHE ? (h0.z & 0xFFu) : h0.z);
         krow[i] = CACHE ? ((h0.z >> 8) & 0xFFu) : static_cast<uint32_t>(i);
-        kgenhi[i] = CACHE ? ((h0.z >> 16) << kGenShift) : genhi;
         kpot[i] = static_cast<int>(h0.w);
 #pragma unroll
-        for (int l0 = 0; l0 < NL; l0 += 4) {
+        for (int l0 = 0; l0 < (CACHE ? 0 : NL); l0 += 4) {
           const uint4 h = *reinterpret_cast<const uint4*>(rr + 4 + l0);
           const uint32_t hv[4] = {h.x, h.y, h.z, h.w};
 #pragma unroll
@@ -875,17 +896,25 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const float x0 = ksc[i] + rD[jj];
           float x1 = x0 + beta;
           if (HAS_LM) {
-            const uint64_t ent = lmrow[CACHE ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e];
-            const uint32_t hi = static_cast<uint32_t>(ent >> 32);
-            float v = rP1[jj];
+            if constexpr (CACHE) {
+              // a cached row holds every token: the fold or the arc, with
+              // the LM target state
+              const uint64_t ent = lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]];
+              x1 = x1 + __uint_as_float(static_cast<uint32_t>(ent));
+              lhi[r] = static_cast<uint32_t>(ent >> 32) & kTargetMask;
+            } else {
+              const uint64_t ent = lmrow[e];
+              const uint32_t hi = static_cast<uint32_t>(ent >> 32);
+              float v = rP1[jj];
 #pragma unroll
-            for (int l = 0; l < NL; ++l) v = v + kbo[i][l];
-            const bool has = hi >= kgenhi[i];
-            const float av = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
-            x1 = x1 + av;
-            // the LM target: with CACHE the entry's own, else its staging
-            // slot (resolved later), or the token's unigram state
-            if constexpr (kKeepLm) lhi[r] = has ? (CACHE ? (hi & kTargetMask) : hi) : rcc[jj];
+              for (int l = 0; l < NL; ++l) v = v + kbo[i][l];
+              const bool has = hi >= genhi;
+              const float av = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
+              x1 = x1 + av;
+              // the LM target: its staging slot (resolved later), or the
+              // token's unigram state
+              if constexpr (kKeepLm) lhi[r] = has ? hi : rcc[jj];
+            }
           }
           if (HAS_BT) {
             const uint32_t be = btrow[e];
@@ -908,8 +937,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         lraw = 0u;
         bk = 0u;
         if (HAS_LM) {
-          const uint32_t hi = static_cast<uint32_t>(lmrow[CACHE ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e] >> 32);
-          lraw = hi >= kgenhi[i] ? (CACHE ? (hi & kTargetMask) : hi) : rcc[jj];
+          if constexpr (CACHE) {
+            lraw = static_cast<uint32_t>(lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]] >> 32) & kTargetMask;
+          } else {
+            const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
+            lraw = hi >= genhi ? hi : rcc[jj];
+          }
         }
         if (HAS_BT) {
           const uint32_t be = btrow[e];
@@ -1192,7 +1225,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             // the best register candidate's fields, tracked by selects so that
             // no candidate array is indexed at run time
             float wx = kNegInf;
-            uint32_t wflat = 0u, wi = 0u, wjj = 0u, wrow = 0u, wgen = 0u;
+            uint32_t wflat = 0u, wi = 0u, wjj = 0u, wrow = 0u;
 #pragma unroll
             for (int r = 0; r < NC; ++r) {
               if (cand[r] != kNegInf) {
@@ -1207,10 +1240,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   wflat = flat;
                   wi = static_cast<uint32_t>(i);
                   wjj = static_cast<uint32_t>(jj);
-                  if constexpr (CACHE) {
-                    wrow = krow[i];
-                    wgen = kgenhi[i];
-                  }
+                  if constexpr (CACHE) wrow = krow[i];
                 }
               }
             }
@@ -1255,8 +1285,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                 uint32_t lmt = 0u, bk = 0u;
                 if (HAS_LM) {
                   if constexpr (CACHE) {
-                    const uint32_t hi = static_cast<uint32_t>(lmrow[wrow * static_cast<uint32_t>(V) + c] >> 32);
-                    lmt = hi >= wgen ? (hi & kTargetMask) : c;
+                    lmt = static_cast<uint32_t>(lmrow[wrow * static_cast<uint32_t>(V) + c] >> 32) & kTargetMask;
                   } else {
                     const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
                     lmt = hi >= genhi ? tgt[hi & 0xFFFu] : c;
@@ -1424,34 +1453,27 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         // KCR empty) through rotations within 16 lanes, lanes 8..15 holding
         // a copy of lanes 0..7.
         const uint32_t st = rec[kRLms];
-        const bool wrap = gen == kGenMax;
-        const uint32_t ngen = wrap ? 1u : gen + 1u;
-        if (wrap) rtag = 0xFFFFFFFFu;
+        if (gen == kGenMax) rtag = 0xFFFFFFFFu;  // the next fill clears every row
         const bool hi8 = lane_in_here<0xFF00FF00FF00FF00ull>();
         const uint32_t rt8 = hi8 ? dpp_row_ror<8>(rtag) : rtag;
-        const uint32_t rg8 = hi8 ? dpp_row_ror<8>(rgen) : rgen;
         const uint32_t ri8 = static_cast<uint32_t>(lane & 7);
         bool hit = false;
-        uint32_t hrow = 0u, hgen = 0u;
-        const auto probe = [&](uint32_t td, uint32_t gd, uint32_t id) __attribute__((always_inline)) {
+        uint32_t hrow = 0u;
+        const auto probe = [&](uint32_t td, uint32_t id) __attribute__((always_inline)) {
           const bool h = st == td;
           hrow = h ? id : hrow;
-          hgen = h ? gd : hgen;
           hit = hit || h;
         };
-        probe(rt8, rg8, ri8);
-        probe(dpp_row_ror<1>(rt8), dpp_row_ror<1>(rg8), dpp_row_ror<1>(ri8));
-        probe(dpp_row_ror<2>(rt8), dpp_row_ror<2>(rg8), dpp_row_ror<2>(ri8));
-        probe(dpp_row_ror<3>(rt8), dpp_row_ror<3>(rg8), dpp_row_ror<3>(ri8));
-        probe(dpp_row_ror<4>(rt8), dpp_row_ror<4>(rg8), dpp_row_ror<4>(ri8));
-        probe(dpp_row_ror<5>(rt8), dpp_row_ror<5>(rg8), dpp_row_ror<5>(ri8));
-        probe(dpp_row_ror<6>(rt8), dpp_row_ror<6>(rg8), dpp_row_ror<6>(ri8));
-        probe(dpp_row_ror<7>(rt8), dpp_row_ror<7>(rg8), dpp_row_ror<7>(ri8));
+        probe(rt8, ri8);
+        probe(dpp_row_ror<1>(rt8), dpp_row_ror<1>(ri8));
+        probe(dpp_row_ror<2>(rt8), dpp_row_ror<2>(ri8));
+        probe(dpp_row_ror<3>(rt8), dpp_row_ror<3>(ri8));
+        probe(dpp_row_ror<4>(rt8), dpp_row_ror<4>(ri8));
+        probe(dpp_row_ror<5>(rt8), dpp_row_ror<5>(ri8));
+        probe(dpp_row_ror<6>(rt8), dpp_row_ror<6>(ri8));
+        probe(dpp_row_ror<7>(rt8), dpp_row_ror<7>(ri8));
         hit = hit && nalive;
-        if (hit) {
-          rowof = static_cast<int>(hrow);
-          rgj = hgen;
-        }
+        if (hit) rowof = static_cast<int>(hrow);
         // rows used by a live slot (slots are lanes 0..7)
         uint32_t ub = hit ? (1u << hrow) : 0u;
         ub |= xor_lane(ub, 1, lane);
@@ -1467,12 +1489,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const bool same = miss && st == sj;
           const int r = min(__builtin_ctz(~used), KCR - 1);  // a free row: < KCR
           used |= 1u << r;
-          if (lane == r) {
-            rtag = sj;
-            rgen = ngen;
-          }
+          if (lane == r) rtag = sj;
           rowof = same ? r : rowof;
-          rgj = same ? ngen : rgj;
           fillrep = fillrep || j == jm;
           miss = miss && !same;
           mm = __ballot(miss);
