@@ -747,6 +747,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         }
         // tiles of 64 arcs never straddle segments: a tile's segment is one
         // ballot away and its fields are wave-uniform (readlane)
+        if (!CACHE || S > 0) {  // uniform; cached rows often need no fill
         const int sincl = wave_incl_scan(static_cast<int>(sg_cnt), lane);
         const uint32_t sstart = static_cast<uint32_t>(sincl) - sg_cnt;  // staging slot of the first arc
         const int stl = static_cast<int>((sg_cnt + 63u) >> 6);
@@ -794,6 +795,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                         (static_cast<unsigned long long>(hi) << 32) | __float_as_uint(av));
             }
           }
+        }
         }
       }
       if (HAS_BT) {
@@ -1499,9 +1501,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       if (wave == 0 && nalive) put_row(lp, 0);
       // chunk plan: live slots in slot order, at most kcmax beams and
       // kLmStage staged arcs per chunk (cached rows stage nothing)
+      if constexpr (CACHE) {
+        nch = na > 0 ? 1 : 0;  // K <= KCR = kcmax, nothing staged
+        cid[0] = 0;
+      } else {
       const int ia = wave_incl_scan(acnt, lane);
       const int tota = rdlane(ia, 63);
-      if (na <= kcmax && (CACHE || tota <= kLmStage)) {
+      if (na <= kcmax && tota <= kLmStage) {
         nch = na > 0 ? 1 : 0;
         cid[0] = 0;
       } else {
@@ -1522,6 +1528,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           ++nch;
           start += cnt;
         }
+      }
       }
     }
     } else {
