@@ -1014,6 +1014,24 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         m1 = fmaxf(m1, xor_lane(m1, 32, lane));
         if (lane < 8) s_top[wave * 8 + lane] = m1;
       }
+      // the blank candidates are exact: with K live slots the smallest blank
+      // score also bounds the K-th best from below (registers only: small
+      // beams take it before the barrier)
+      const auto blank_bound = [&]() __attribute__((always_inline)) {
+        float tb = (lane < K) ? sc[0] + rBlank : __builtin_huge_valf();
+#pragma unroll
+        for (int h = 1; h < SPL; ++h)
+          if (j + 64 * h < K) tb = fmin_sel(tb, sc[h] + rBlank);
+        tb = fmin_sel(tb, xor_lane(tb, 1, lane));
+        tb = fmin_sel(tb, xor_lane(tb, 2, lane));
+        tb = fmin_sel(tb, xor_lane(tb, 4, lane));
+        if (K > 8) tb = fmin_sel(tb, xor_lane(tb, 8, lane));
+        if (K > 16) tb = fmin_sel(tb, xor_lane(tb, 16, lane));
+        if (K > 32) tb = fmin_sel(tb, xor_lane(tb, 32, lane));
+        return rdlane(tb, 0);
+      };
+      float tblank = 0.0f;
+      if constexpr (kSmallK) tblank = blank_bound();
       __syncthreads();  // B: bound inputs, blanks, pool reset
 
       // ---- T. bound and filter ----
@@ -1028,7 +1046,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           rw = fmaxf(rw, xor_lane(rw, 8, lane));
           rw = fmaxf(rw, xor_lane(rw, 16, lane));  // lanes 0..31: waves 0..3, lanes 32..63: 4..7
           const float oh = xor_lane(rw, 32, lane);
-          float v = lane_in(0xFFull) ? rw : (lane_in(0xFF00ull) ? oh : (lane_in(0xFF0000ull) ? wm : kNegInf));
+          // plain selects (a nested conditional became branches, with the
+          // wave-maxima read moved into one of them)
+          float v = kNegInf;
+          v = lane_in(0xFF0000ull) ? wm : v;
+          v = lane_in(0xFF00ull) ? oh : v;
+          v = lane_in(0xFFull) ? rw : v;
           v = wave_sort_desc<16>(v, lane);
           tc = fmaxf(rdlane(v, K - 1), rdlane(v, 16 + K - 1));
         } else if (SPL == 1) {
@@ -1064,19 +1087,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           for (int d = 1; d < 64; d <<= 1) v = fmax_sel(v, xor_lane(v, d, lane));
           tc = v;
         }
-        // the blank candidates are exact: with K live slots the smallest
-        // blank score also bounds the K-th best from below
-        float tb = (lane < K) ? sc[0] + rBlank : __builtin_huge_valf();
-#pragma unroll
-        for (int h = 1; h < SPL; ++h)
-          if (j + 64 * h < K) tb = fmin_sel(tb, sc[h] + rBlank);
-        tb = fmin_sel(tb, xor_lane(tb, 1, lane));
-        tb = fmin_sel(tb, xor_lane(tb, 2, lane));
-        tb = fmin_sel(tb, xor_lane(tb, 4, lane));
-        if (K > 8) tb = fmin_sel(tb, xor_lane(tb, 8, lane));
-        if (K > 16) tb = fmin_sel(tb, xor_lane(tb, 16, lane));
-        if (K > 32) tb = fmin_sel(tb, xor_lane(tb, 32, lane));
-        const float tblank = rdlane(tb, 0);
+        if constexpr (!kSmallK) tblank = blank_bound();
         // an infinite bound admits every finite candidate and no -inf one
         const float tau = fmaxf(fmaxf(fmaxf(tau_run, tc), tblank), -__FLT_MAX__);
         // most waves hold no survivor: their lane maxima say so
