@@ -1217,14 +1217,21 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               const bool win = (lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf;
               uint32_t lmt = eq.z;
               if (HAS_LM && !SKIP && !CACHE && win && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
-              if (last_chunk) {
-                Succ sp;
-                succ_begin(win, eq.y, lmt, eq.w, prec, sp);
-                succ_end(sp, eq.x);
-                if (win) store_rec(nrec + myrank * RW, sp.r);
-              } else if (win) {
-                s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
-              }
+              // winners to region Q in rank order (after the last chunk their
+              // successor records are built below, in one pass)
+              if (win) s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
+            }
+            if (last_chunk) {
+              __syncthreads();  // region Q complete
+              // rank tid (waves 0 .. SPL-1): the chain-header loads of all
+              // winners are in flight together
+              const bool act = (SPL > 1 || wave == 0) && tid < min(K, nfin);
+              uint4 e = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+              if (act) e = s_res[Q][tid];
+              Succ sp;
+              succ_begin(act, e.y, e.z, e.w, prec, sp);
+              succ_end(sp, e.x);
+              if (act) store_rec(nrec + tid * RW, sp.r);
             }
           }
         } else {
