@@ -368,7 +368,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // for two or more labels per lane
   constexpr bool kSmallK = SPL == 1 && !SKIP && LPT >= 2;
   static_assert(!CACHE || (kSmallK && HAS_LM && NL > 0 && !HAS_BT), "row caching needs one chunk and an LM");
-  constexpr int kRowWords = 16;               // beam record per live position
+  // The key rows hold the unigram + backoff fold of every token (as order-0
+  // entries) with row caching, and for chains of four or more levels with
+  // one slot per lane, whose backoff weights would otherwise take KCR x NL
+  // registers in the scoring.  Shorter chains, and the many chunks of two
+  // slots per lane, fold in the scoring: cheaper than the extra LDS maxima.
+  constexpr bool kFoldRows = CACHE || (NL >= 4 && SPL == 1);
+  constexpr int kRowWords = kFoldRows ? 4 : 16;  // beam record per live position
   // beam state record (one per slot, double-buffered by frame): score bits,
   // back-pointer, transcript hash (2), length, last label, LM state, boosting
   // state, emitted flag, boosting list begin/count/pot, LM chain begin[NL],
@@ -383,7 +389,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   static_assert(kCap / 2 <= kThreads, "the fallback reads carried pool entries one per thread");
   // reserved regions (ping-pong): blank candidates, or the best K so far
   __shared__ uint4 s_res[2][KMX];
-  // beam records by live position: score, last label, slot, pot, backoff weights
+  // beam records by live position: score, last label, slot (and key row),
+  // boosting pot, backoff weights unless the rows hold the fold; reused by
+  // the epilogue (lengths and ranks, 2 KMX words)
   __shared__ __align__(16) uint32_t s_row[(KMX + 16) * kRowWords];
   // beam state records by slot: [rcur] the current beam, [rcur ^ 1] its successors
   __shared__ __align__(16) uint32_t s_rec[2 * KMX * RW];
@@ -400,6 +408,14 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   uint64_t* const lmrow = reinterpret_cast<uint64_t*>(s_big);
   uint32_t* const btrow = s_big + kOffBtRow;
   uint32_t* const tgt = s_big + kOffTgt;
+  // LM target of an uncached row entry (or of a pool entry's raw field): an
+  // explicit arc (order >= 1) names its staging slot; a fold entry (order 0)
+  // or, in rows without folds, a bare token names the token, whose unigram
+  // state has the token's id
+  const auto lm_target = [&](uint32_t hi) __attribute__((always_inline)) {
+    if constexpr (kFoldRows) return ((hi >> 23) & 7u) != 0u ? tgt[hi & 0xFFFu] : (hi & 0xFFFu);
+    else return (hi >> kGenShift) != 0u ? tgt[hi & 0xFFFu] : hi;
+  };
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -497,7 +513,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc[h]), static_cast<uint32_t>(last[h]),
                                                zf, static_cast<uint32_t>(btpot[h]));
 #pragma unroll
-    for (int l0 = 0; l0 < NL; l0 += 4) {
+    for (int l0 = 0; l0 < (kFoldRows ? 0 : NL); l0 += 4) {
       const auto bo_at = [&](int l) __attribute__((always_inline)) { return l < NL ? __float_as_uint(lvbo[h][l < NLA ? l : 0]) : 0u; };
       *reinterpret_cast<uint4*>(rr + 4 + l0) = make_uint4(bo_at(l0), bo_at(l0 + 1), bo_at(l0 + 2), bo_at(l0 + 3));
     }
@@ -720,6 +736,34 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
           }
         }
+        if constexpr (!CACHE && kFoldRows) {
+          // every token of every row of the chunk gets its unigram + backoff
+          // fold as an order-0 entry holding the token (its unigram state);
+          // the explicit arcs (order >= 1) win the maximum
+#pragma unroll
+          for (int h = 0; h < SPL; ++h) {
+            uint64_t fm = __ballot(inch[h]);
+            while (fm != 0ull) {  // uniform
+              const int jr = static_cast<int>(__builtin_ctzll(fm));
+              fm &= fm - 1ull;
+              const uint32_t rf = rdlane(static_cast<uint32_t>(row[h]), jr);
+              float bo[NLA];
+#pragma unroll
+              for (int l = 0; l < NL; ++l) bo[l] = rdlane(lvbo[h][l], jr);
+#pragma unroll
+              for (int jj = 0; jj < LPT; ++jj) {
+                if (tid + jj * kThreads < V) {
+                  float v = rP1[jj];
+#pragma unroll
+                  for (int l = 0; l < NL; ++l) v = v + bo[l];
+                  const float av = alpha * v;
+                  atomicMax(reinterpret_cast<unsigned long long*>(&lmrow[rf * static_cast<uint32_t>(V) + rcc[jj]]),
+                            (static_cast<unsigned long long>(genhi | rcc[jj]) << 32) | __float_as_uint(av));
+                }
+              }
+            }
+          }
+        }
         if constexpr (CACHE) {
           // every token of a new row gets its unigram + backoff fold as an
           // order-0 entry (the explicit arcs, order >= 1, win the maximum),
@@ -859,7 +903,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       int kslot[KCR];
       float ksc[KCR];
       int klast[KCR];
-      float kbo[KCR][NLA];
+      float kbo[KCR][NLA];  // backoff weights (rows without the fold)
       int kpot[KCR];
       // LM key row of chunk row i
       uint32_t krow[KCR];
@@ -873,7 +917,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         krow[i] = CACHE ? ((h0.z >> 8) & 0xFFu) : static_cast<uint32_t>(i);
         kpot[i] = static_cast<int>(h0.w);
 #pragma unroll
-        for (int l0 = 0; l0 < (CACHE ? 0 : NL); l0 += 4) {
+        for (int l0 = 0; l0 < (kFoldRows ? 0 : NL); l0 += 4) {
           const uint4 h = *reinterpret_cast<const uint4*>(rr + 4 + l0);
           const uint32_t hv[4] = {h.x, h.y, h.z, h.w};
 #pragma unroll
@@ -904,6 +948,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               const uint64_t ent = lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]];
               x1 = x1 + __uint_as_float(static_cast<uint32_t>(ent));
               lhi[r] = static_cast<uint32_t>(ent >> 32) & kTargetMask;
+            } else if constexpr (kFoldRows) {
+              // the chunk's rows hold every token: the fold (order 0, the
+              // token) or an explicit arc (its staging slot, resolved later)
+              const uint64_t ent = lmrow[e];
+              x1 = x1 + __uint_as_float(static_cast<uint32_t>(ent));
+              if constexpr (kKeepLm) lhi[r] = static_cast<uint32_t>(ent >> 32);
             } else {
               const uint64_t ent = lmrow[e];
               const uint32_t hi = static_cast<uint32_t>(ent >> 32);
@@ -913,8 +963,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               const bool has = hi >= genhi;
               const float av = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
               x1 = x1 + av;
-              // the LM target: its staging slot (resolved later), or the
-              // token's unigram state
+              // the LM target: an explicit arc's staging slot (resolved
+              // later), or the token's unigram state
               if constexpr (kKeepLm) lhi[r] = has ? hi : rcc[jj];
             }
           }
@@ -943,7 +993,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             lraw = static_cast<uint32_t>(lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]] >> 32) & kTargetMask;
           } else {
             const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
-            lraw = hi >= genhi ? hi : rcc[jj];
+            lraw = (kFoldRows || hi >= genhi) ? hi : rcc[jj];
           }
         }
         if (HAS_BT) {
@@ -1118,7 +1168,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                 } else {
                   cand_meta(i, jj, lraw, bk);
                 }
-                if (HAS_LM && SKIP && (lraw >> kGenShift) != 0u) lraw = tgt[lraw & 0xFFFu];
+                if (HAS_LM && SKIP && !CACHE) lraw = lm_target(lraw);
                 s_pool[slot] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lraw, bk);
               } else {
                 s_overflow = 1;
@@ -1159,7 +1209,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             nfin = __popcll(__ballot(xq != kNegInf));
             const bool own = ((lane & (kWaves - 1)) == wave) && xq != kNegInf;
             uint32_t lmt = eq.z;
-            if (HAS_LM && !SKIP && !CACHE && lane >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+            if (HAS_LM && !SKIP && !CACHE && lane >= K) lmt = lm_target(lmt);
             Succ sp;
             if (last_chunk) succ_begin(own, eq.y, lmt, eq.w, prec, sp);  // loads overlap the ranking
             int myrank = K;
@@ -1216,7 +1266,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               for (int u = 0; u < 8; ++u) myrank = ((lane >> 3) == u) ? rk[u] : myrank;
               const bool win = (lane & (kWaves - 1)) == wave && myrank < K && xq != kNegInf;
               uint32_t lmt = eq.z;
-              if (HAS_LM && !SKIP && !CACHE && win && q >= K && (lmt >> kGenShift) != 0u) lmt = tgt[lmt & 0xFFFu];
+              if (HAS_LM && !SKIP && !CACHE && win && q >= K) lmt = lm_target(lmt);
               // winners to region Q in rank order (after the last chunk their
               // successor records are built below, in one pass)
               if (win) s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
@@ -1308,7 +1358,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                     lmt = static_cast<uint32_t>(lmrow[wrow * static_cast<uint32_t>(V) + c] >> 32) & kTargetMask;
                   } else {
                     const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
-                    lmt = hi >= genhi ? tgt[hi & 0xFFFu] : c;
+                    lmt = (kFoldRows || hi >= genhi) ? lm_target(hi) : c;
                   }
                 }
                 if (HAS_BT) {
