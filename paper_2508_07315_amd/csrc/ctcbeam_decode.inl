@@ -31,15 +31,19 @@
 //      slot : alpha*value) combined with an atomic max, so the highest-order
 //      n-gram wins in any order; boosting entries are generation-tagged keys.
 //      Entries of older generations read as absent, so the rows are never
-//      cleared (except when the 6-bit generation wraps).
+//      cleared (except when the 6-bit generation wraps).  For small beams
+//      with an LM and no boosting the rows are kept per LM state across
+//      frames and only states new to the rows are filled (CACHE); those rows,
+//      and the rows of chains of four or more levels, also get the unigram +
+//      backoff fold of every token as an order-0 entry.
 //   C. candidates: each lane scores its labels for every beam of the chunk in
 //      registers (beam data by broadcast LDS reads), resolving the LM value
 //      from the row or from the unigram + backoff fold, and publishes the
-//      maxima of disjoint lane groups.
-//   T. filter: the K-th largest group maximum, and with K live slots the
-//      smallest blank score, bound the K-th best candidate from below;
-//      candidates at or above the bound (a few dozen) go to a survivor pool
-//      in LDS.
+//      maxima of disjoint (beam row, lane group) candidate groups.
+//   T. filter: the K-th largest group maximum (over the frame's chunks so
+//      far), and with K live slots the smallest blank score, bound the K-th
+//      best candidate from below; candidates at or above the bound (a few on
+//      the 3-gram workload) go to a survivor pool in LDS.
 //   R. rank: the pool (survivors plus K reserved entries holding the blank
 //      candidates, or the best K of earlier chunks) is ranked exactly by
 //      (score desc, flat index asc): each wave ranks an eighth of the pool
@@ -49,9 +53,9 @@
 //      fetched while the ranking runs).
 //   U. update: prune, recombine, take the new beam into registers, plan the
 //      next frame's chunks, write back-pointers to HBM.
-// Large beams (K*V above the key rows) repeat F/C/T/R per chunk of beams with
-// a running bound.  A survivor pool overflow falls back to an exact
-// extraction.  After the last frame the best beam is traced back through the
+// Large beams (K*V above the key rows) repeat F/C/T per chunk of beams with
+// a running bound and rank the pool only when it fills up or after the last
+// chunk.  A survivor pool overflow falls back to an exact extraction.  After the last frame the best beam is traced back through the
 // back-pointers staged in LDS.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
