@@ -336,6 +336,33 @@ __device__ __forceinline__ bool dup_by_sort(uint64_t key, int lane, uint32_t& lo
   return __builtin_amdgcn_ds_permute(static_cast<int>(sl) << 2, d ? 1 : 0) != 0;
 }
 
+// Count, per lane, the values of its 16-lane row at least as large as its own
+// (the lane itself included): 15 rotations, no dependent sort.
+template <int D>
+__device__ __forceinline__ uint32_t ge_count_step(float v, uint32_t n) {
+  const float o = __uint_as_float(dpp_row_ror<D>(__float_as_uint(v)));
+  return n + (o >= v ? 1u : 0u);
+}
+__device__ __forceinline__ uint32_t row_ge_count(float v) {
+  uint32_t n = 1u;
+  n = ge_count_step<1>(v, n);
+  n = ge_count_step<2>(v, n);
+  n = ge_count_step<3>(v, n);
+  n = ge_count_step<4>(v, n);
+  n = ge_count_step<5>(v, n);
+  n = ge_count_step<6>(v, n);
+  n = ge_count_step<7>(v, n);
+  n = ge_count_step<8>(v, n);
+  n = ge_count_step<9>(v, n);
+  n = ge_count_step<10>(v, n);
+  n = ge_count_step<11>(v, n);
+  n = ge_count_step<12>(v, n);
+  n = ge_count_step<13>(v, n);
+  n = ge_count_step<14>(v, n);
+  n = ge_count_step<15>(v, n);
+  return n;
+}
+
 // Bitonic sort of one value per lane within groups of N lanes, descending.
 template <int N>
 __device__ __forceinline__ float wave_sort_desc(float v, int lane) {
@@ -371,6 +398,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // without rank skipping the beam fits one chunk of 16 / LPT rows: K <= 8
   // for two or more labels per lane
   constexpr bool kSmallK = SPL == 1 && !SKIP && LPT >= 2;
+  // rank skipping means K > 16 / LPT: no beam of at most 8 for LPT <= 2
+  constexpr bool kMaySmallK = !SKIP || LPT > 2;
   static_assert(!CACHE || (kSmallK && HAS_LM && NL > 0 && !HAS_BT), "row caching needs one chunk and an LM");
   // The key rows hold the unigram + backoff fold of every token (as order-0
   // entries) with row caching, and for chains of four or more levels with
@@ -1043,7 +1072,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         // at each of the lane-bit steps 1, 2, 4, leaving lane l with group
         // 4(l&1) + 2(l>>1&1) + (l>>2&1), then reduces over lane bits 3..5.
         // K <= 8 also keeps the 8 wave maxima.
-        if (kSmallK || K <= 8) {
+        if (kSmallK || (kMaySmallK && K <= 8)) {
           const float g = row_max_last(lmax);
           const float g2 = fmax_sel(fmax_sel(rdlane(g, 15), rdlane(g, 31)), fmax_sel(rdlane(g, 47), rdlane(g, 63)));
           if (lane == 0) s_top[kWaves * 8 + wave] = g2;
@@ -1091,7 +1120,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       // ---- T. bound and filter ----
       {
         float tc;
-        if (kSmallK || K <= 8) {
+        if (kSmallK || (kMaySmallK && K <= 8)) {
           // two bounds sorted side by side in groups of 16 lanes: lanes 0..15
           // the maxima of (row, half of the waves), lanes 16..23 the wave
           // maxima
@@ -1106,8 +1135,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           v = lane_in(0xFF0000ull) ? wm : v;
           v = lane_in(0xFF00ull) ? oh : v;
           v = lane_in(0xFFull) ? rw : v;
-          v = wave_sort_desc<16>(v, lane);
-          tc = fmaxf(rdlane(v, K - 1), rdlane(v, 16 + K - 1));
+          // the K-th largest of each 16-lane row: the largest value with at
+          // least K values of its row at or above it
+          const float kv = row_max_last(row_ge_count(v) >= static_cast<uint32_t>(K) ? v : kNegInf);
+          tc = fmaxf(rdlane(kv, 15), rdlane(kv, 31));
         } else if (SPL == 1) {
           // this chunk's 64 (row group, wave) maxima, sorted ascending, merged
           // into the frame's running top 64 (descending): the elementwise
