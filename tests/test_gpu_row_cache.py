@@ -10,7 +10,9 @@ both match the CPU oracle (tokens bit-exact, scores within 1e-4).
   6-bit row generation wraps six times per utterance);
 * 1-best and N-best, max and log-sum-exp recombination, theta = inf and 12;
 * fuzzing over V (all three row counts), LM order 2..6 and K;
-* the full-size comparison of the two paths (no oracle: too slow there).
+* the full-size comparison of the two paths (no oracle: too slow there);
+* an LM of more than 2^23 states (the paper-scale 6-gram) takes the refill
+  path with the same results.
 """
 import math
 
@@ -121,3 +123,20 @@ def test_row_cache_fuzz(seed):
     r = oracle.decode(lp, lens, K, alpha, beta, 0.0, theta=theta, lm=olm,
                       n_threads=oracle_threads(), logsumexp=lse)
     compare(g, r, what=f"row cache fuzz {seed}")
+
+
+def test_large_lm_takes_the_refill_path():
+    # the 6-gram of the paper-scale workload numbers 8.5 M LM states, above
+    # the 2^23 a cached entry can name: small beams without boosting refill
+    # their rows every frame; results as with the flag, and the oracle's
+    w = W.CONFIGS[6].replace(B=2, T=80, lengths=("uniform", 50, 80), K=8, boost=None, boost_w=0.0)
+    lm, _, olm, _ = handles(w)
+    lp = W.make_logprobs(w)
+    lens = W.make_lengths(w)
+    log("6-gram without boosting, K=8 (LM above 2^23 states)")
+    g = _run(lp, lens, 8, w.alpha, w.beta, lm, theta=w.theta)
+    g0 = _run(lp, lens, 8, w.alpha, w.beta, lm, theta=w.theta, row_cache=False)
+    _same(g, g0, "large LM default vs refill flag")
+    r = oracle.decode(lp, lens, 8, w.alpha, w.beta, 0.0, theta=w.theta, lm=olm,
+                      n_threads=oracle_threads())
+    compare(g, r, what="large LM K=8")
