@@ -409,12 +409,16 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool kFoldRows = CACHE || (NL >= 4 && SPL == 1);
   constexpr int kRowWords = kFoldRows ? 4 : 16;  // beam record per live position
   // beam state record (one per slot, double-buffered by frame): score bits,
-  // back-pointer, transcript hash (2), length, last label, LM state, boosting
-  // state, emitted flag, boosting list begin/count/pot, LM chain begin[NL],
-  // count[NL], backoff[NL]
-  constexpr int kRX = 0, kRBp = 1, kRHlo = 2, kRHhi = 3, kRLen = 4, kRLast = 5, kRLms = 6, kRBts = 7;
-  constexpr int kREmit = 8, kRBtb = 9, kRBtc = 10, kRBtp = 11, kRLvb = 12, kRLvc = 12 + NL, kRLvbo = 12 + 2 * NL;
-  constexpr int RW = (12 + 3 * NL + 3) & ~3;
+  // back-pointer, transcript hash (2), length, last label, LM state, then
+  // with boosting: boosting state, emitted flag, boosting list
+  // begin/count/pot; without: emitted flag; then LM chain begin[NL],
+  // count[NL], backoff[NL].  The boosting fields exist (and are accessed)
+  // only with boosting.
+  constexpr int kRX = 0, kRBp = 1, kRHlo = 2, kRHhi = 3, kRLen = 4, kRLast = 5, kRLms = 6;
+  constexpr int kRBts = 7, kRBtb = 9, kRBtc = 10, kRBtp = 11;
+  constexpr int kREmit = HAS_BT ? 8 : 7;
+  constexpr int kRLvb = HAS_BT ? 12 : 8, kRLvc = kRLvb + NL, kRLvbo = kRLvb + 2 * NL;
+  constexpr int RW = (kRLvb + 3 * NL + 3) & ~3;
 
   __shared__ __align__(16) uint32_t s_big[kBigWords];
   // survivor pool: score bits, flat index, LM target (raw), boosting key
@@ -639,9 +643,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     for (int w = 0; w < RW; ++w) r[w] = 0u;
     r[kRLast] = static_cast<uint32_t>(V);
     r[kRLms] = HAS_LM ? p.lm_bos_state : 0u;
-    r[kRBtb] = btb[0];
-    r[kRBtc] = btc[0];
-    r[kRBtp] = static_cast<uint32_t>(btpot[0]);
+    if (HAS_BT) {
+      r[kRBtb] = btb[0];
+      r[kRBtc] = btc[0];
+      r[kRBtp] = static_cast<uint32_t>(btpot[0]);
+    }
 #pragma unroll
     for (int l = 0; l < NL; ++l) {
       r[kRLvb + l] = lvb[0][l];
