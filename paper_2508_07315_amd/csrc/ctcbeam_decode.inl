@@ -1193,28 +1193,39 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           if (lane == 0) wbase = atomicAdd(&s_nbuf, wtotal);
           wbase = __builtin_amdgcn_readfirstlane(wbase);
           int slot = wbase + incl - mycnt;
+          // the pool entry of candidate r (LM target: the staged arc's or the
+          // token's unigram state; with rank skipping resolved now, as a
+          // later chunk reuses the staging area before the rank, otherwise
+          // by the rank)
+          const auto put = [&](int r, int at) __attribute__((always_inline)) {
+            const int i = r / LPT, jj = r % LPT;
+            const int c = tid + jj * kThreads;
+            uint32_t lraw, bk;
+            if constexpr (kKeepLm) {
+              lraw = lhi[r];
+              bk = 0u;
+            } else {
+              cand_meta(i, jj, lraw, bk);
+            }
+            if (HAS_LM && SKIP && !CACHE) lraw = lm_target(lraw);
+            s_pool[at] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lraw, bk);
+          };
+          if (wbase + wtotal <= kCap) {  // uniform: the wave's range fits
 #pragma unroll
-          for (int r = 0; r < NC; ++r) {
-            if (qmask & (1u << r)) {
-              if (slot < kCap) {
-                const int i = r / LPT, jj = r % LPT;
-                const int c = tid + jj * kThreads;
-                // LM target: the staged arc's or the token's unigram state.
-                // With rank skipping it is resolved now (a later chunk reuses
-                // the staging area before the rank), otherwise by the rank.
-                uint32_t lraw, bk;
-                if constexpr (kKeepLm) {
-                  lraw = lhi[r];
-                  bk = 0u;
-                } else {
-                  cand_meta(i, jj, lraw, bk);
-                }
-                if (HAS_LM && SKIP && !CACHE) lraw = lm_target(lraw);
-                s_pool[slot] = make_uint4(__float_as_uint(cand[r]), static_cast<uint32_t>(kslot[i] * W + c), lraw, bk);
-              } else {
-                s_overflow = 1;
+            for (int r = 0; r < NC; ++r) {
+              if (qmask & (1u << r)) {
+                put(r, slot);
+                ++slot;
               }
-              ++slot;
+            }
+          } else {
+#pragma unroll
+            for (int r = 0; r < NC; ++r) {
+              if (qmask & (1u << r)) {
+                if (slot < kCap) put(r, slot);
+                else s_overflow = 1;
+                ++slot;
+              }
             }
           }
         }
