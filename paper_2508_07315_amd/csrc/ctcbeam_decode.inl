@@ -400,6 +400,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool kSmallK = SPL == 1 && !SKIP && LPT >= 2;
   // rank skipping means K > 16 / LPT: no beam of at most 8 for LPT <= 2
   constexpr bool kMaySmallK = !SKIP || LPT > 2;
+  // LM arc tiles in flight per wave: cached rows fill only the new states
+  constexpr int kLmTU = CACHE ? 4 : kTileUnroll;
   static_assert(!CACHE || (kSmallK && HAS_LM && NL > 0 && !HAS_BT), "row caching needs one chunk and an LM");
   // The key rows hold the unigram + backoff fold of every token (as order-0
   // entries) with row caching, and for chains of four or more levels with
@@ -837,12 +839,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         const int tincl = wave_incl_scan(stl, lane);
         const int texcl = tincl - stl;
         const int ntile = rdlane(tincl, 63);
-        for (int t0 = wave; t0 < ntile; t0 += kWaves * kTileUnroll) {
-          LmArc a[kTileUnroll];
-          uint32_t apos[kTileUnroll], arl[kTileUnroll];
-          float af[kTileUnroll][NF];
+        for (int t0 = wave; t0 < ntile; t0 += kWaves * kLmTU) {
+          LmArc a[kLmTU];
+          uint32_t apos[kLmTU], arl[kLmTU];
+          float af[kLmTU][NF];
 #pragma unroll
-          for (int u = 0; u < kTileUnroll; ++u) {
+          for (int u = 0; u < kLmTU; ++u) {
             const int tt = t0 + u * kWaves;
             apos[u] = 0xFFFFFFFFu;
             arl[u] = 0u;
@@ -859,7 +861,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
           }
 #pragma unroll
-          for (int u = 0; u < kTileUnroll; ++u) {
+          for (int u = 0; u < kLmTU; ++u) {
             const uint32_t q = apos[u];
             // positions past a segment's arcs (and tiles past the last) skip
             if (q != 0xFFFFFFFFu && a[u].token < static_cast<uint32_t>(V)) {
