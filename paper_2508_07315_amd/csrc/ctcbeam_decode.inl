@@ -1079,12 +1079,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         // 16 rows): a transposed reduction halves the groups a lane carries
         // at each of the lane-bit steps 1, 2, 4, leaving lane l with group
         // 4(l&1) + 2(l>>1&1) + (l>>2&1), then reduces over lane bits 3..5.
-        // K <= 8 also keeps the 8 wave maxima.
-        if (kSmallK || (kMaySmallK && K <= 8)) {
-          const float g = row_max_last(lmax);
-          const float g2 = fmax_sel(fmax_sel(rdlane(g, 15), rdlane(g, 31)), fmax_sel(rdlane(g, 47), rdlane(g, 63)));
-          if (lane == 0) s_top[kWaves * 8 + wave] = g2;
-        }
+        // K <= 8 also keeps the 8 wave maxima (the maximum of the 8 row
+        // groups below).
         float m8[8];
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -1104,6 +1100,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         m1 = fmaxf(m1, xor_lane(m1, 16, lane));
         m1 = fmaxf(m1, xor_lane(m1, 32, lane));
         if (lane < 8) s_top[wave * 8 + lane] = m1;
+        if (kSmallK || (kMaySmallK && K <= 8)) {
+          float wm = fmaxf(m1, xor_lane(m1, 1, lane));
+          wm = fmaxf(wm, xor_lane(wm, 2, lane));
+          wm = fmaxf(wm, xor_lane(wm, 4, lane));
+          if (lane == 0) s_top[kWaves * 8 + wave] = wm;
+        }
       }
       // the blank candidates are exact: with K live slots the smallest blank
       // score also bounds the K-th best from below (registers only: small
