@@ -1018,9 +1018,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           }
           const float x = (c != klast[i]) ? x1 : x0;
           cand[r] = x;
-          lmax = fmaxf(lmax, x);
           rmax[i] = jj == 0 ? x : fmaxf(rmax[i], x);
         }
+        lmax = fmaxf(lmax, rmax[i]);
       }
       // LM entry (staged, or the token's unigram state) and boosting key of
       // candidate (i, jj), re-read from the rows for the few that are kept
