@@ -44,6 +44,16 @@ def test_exports_every_declared_symbol():
     assert not missing, missing
 
 
+def test_flag_values_match_the_header():
+    # the binding's option bits are the header's CTCBEAM_FLAG_* values
+    hdr = open(os.path.join(ROOT, "include", "ctcbeam.h")).read()
+    flags = {m.group(1): int(m.group(2)) for m in re.finditer(r"#define CTCBEAM_FLAG_(\w+)\s+(\d+)", hdr)}
+    assert flags == {"LOGSUMEXP": P.FLAG_LOGSUMEXP, "BOOST_ROLLBACK": P.FLAG_BOOST_ROLLBACK,
+                     "NO_ROW_CACHE": P.FLAG_NO_ROW_CACHE}, flags
+    assert len(set(flags.values())) == len(flags)
+    assert all(v & (v - 1) == 0 for v in flags.values())  # one bit each
+
+
 # ---------------------------------------------------------------------------
 # LM tables
 # ---------------------------------------------------------------------------
