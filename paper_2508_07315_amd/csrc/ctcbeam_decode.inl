@@ -402,6 +402,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool kMaySmallK = !SKIP || LPT > 2;
   // LM arc tiles in flight per wave: cached rows fill only the new states
   constexpr int kLmTU = CACHE ? 4 : kTileUnroll;
+  // boosting continuation tiles in flight per wave (a few dozen arcs a frame)
+  constexpr int kBtTU = 2;
   static_assert(!CACHE || (kSmallK && HAS_LM && NL > 0 && !HAS_BT), "row caching needs one chunk and an LM");
   // The key rows hold the unigram + backoff fold of every token (as order-0
   // entries) with row caching, and for chains of four or more levels with
@@ -911,12 +913,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const int tincl = wave_incl_scan(btl, lane);
           const int texcl = tincl - btl;
           const int ntile = rdlane(tincl, 63);
-          for (int t0 = wave; t0 < ntile; t0 += kWaves * kTileUnroll) {
-            BtEntry e[kTileUnroll];
-            uint32_t erow[kTileUnroll];
-            bool eok[kTileUnroll];
+          for (int t0 = wave; t0 < ntile; t0 += kWaves * kBtTU) {
+            BtEntry e[kBtTU];
+            uint32_t erow[kBtTU];
+            bool eok[kBtTU];
 #pragma unroll
-            for (int u = 0; u < kTileUnroll; ++u) {
+            for (int u = 0; u < kBtTU; ++u) {
               const int tt = t0 + u * kWaves;
               erow[u] = 0u;
               eok[u] = false;
@@ -930,7 +932,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               }
             }
 #pragma unroll
-            for (int u = 0; u < kTileUnroll; ++u)
+            for (int u = 0; u < kBtTU; ++u)
               if (eok[u] && e[u].token < static_cast<uint32_t>(V))
                 btrow[erow[u] * V + e[u].token] = (e[u].key & kLowMask) | genhi;
           }
