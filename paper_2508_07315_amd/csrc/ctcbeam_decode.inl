@@ -402,8 +402,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool kMaySmallK = !SKIP || LPT > 2;
   // LM arc tiles in flight per wave: cached rows fill only the new states
   constexpr int kLmTU = CACHE ? 4 : kTileUnroll;
-  // boosting continuation tiles in flight per wave (a few dozen arcs a frame)
-  constexpr int kBtTU = 2;
+  // boosting continuation tiles in flight per wave (a few dozen arcs a frame:
+  // more tiles only add registers)
+  constexpr int kBtTU = 1;
   static_assert(!CACHE || (kSmallK && HAS_LM && NL > 0 && !HAS_BT), "row caching needs one chunk and an LM");
   // The key rows hold the unigram + backoff fold of every token (as order-0
   // entries) with row caching, and for chains of four or more levels with
