@@ -17,7 +17,10 @@ Prints ONE JSON line:
                4 B per emitting winner; per utterance 8*V staging + 4*T + 4
                output bytes.
   cpu_baseline = the CPU oracle timed on a bounded sample of the same
-               workload (a reported baseline, not a target).
+               workload (a reported baseline, not a target): one warm-up and
+               the median of 5 runs, on 1 thread and on up to 16 threads
+               (one utterance each), with the host's CPU model and nproc.
+  config.theta is null when there is no pruning (theta = +inf).
 
 --mode nbest times the N-best entry point on the same workload (all K final
 hypotheses out); --mode greedy times greedy decoding with the same LM fusion
@@ -87,26 +90,64 @@ def load_traffic(workload: str, mode: str = "beam"):
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, lp, lens, n_utts: int, threads: int, mode: str = "beam"):
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _usable_cores() -> int:
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def cpu_baseline(w, lp, lens, threads: int, mode: str = "beam", reps: int = 5):
+    """The CPU oracle on the host cores, timed as the survey's protocol asks:
+    one warm-up run, then the median of ``reps`` runs, (i) on one thread over
+    one utterance and (ii) on ``threads`` threads over ``threads`` utterances
+    (one per thread), wall time by time.perf_counter.  Frames/s counts padded
+    frames (B*T), like the GPU metric."""
     import numpy as np
 
     import oracle
     import workloads as W
-    idx = list(range(min(n_utts, w.B)))
     lm = oracle.LM(W.lm_for(w.lm, w.V)) if w.lm is not None else None
     bt = None
     if w.boost is not None:
         off, tok = W.phrases_for(w.boost, w.V)
         bt = oracle.BT(w.V, off, tok)
-    t0 = time.perf_counter()
-    oracle.decode(lp[idx], lens[idx], 1 if mode == "greedy" else w.K, w.alpha, w.beta, w.boost_w,
-                  theta=w.theta, lm=lm, bt=bt, n_threads=threads, want_nbest=mode == "nbest")
-    dt = time.perf_counter() - t0
-    frames = len(idx) * w.T
-    return dict(value=frames / dt, unit="frames/s", cores=min(threads, len(idx)), kind="oracle",
-                sample=f"{len(idx)} of {w.B} utterances ({int(np.sum(lens[idx]))} valid frames, "
-                       f"T={w.T} padded) of the same workload, {dt:.2f} s wall",
-                valid_frames_per_s=float(np.sum(lens[idx])) / dt)
+    K = 1 if mode == "greedy" else w.K
+
+    def timed(n_threads):
+        idx = list(range(min(n_threads, w.B)))
+        x, ln = np.ascontiguousarray(lp[idx]), lens[idx]
+        ts = []
+        for r in range(reps + 1):  # run 0 is the warm-up
+            t0 = time.perf_counter()
+            oracle.decode(x, ln, K, w.alpha, w.beta, w.boost_w, theta=w.theta, lm=lm, bt=bt,
+                          n_threads=n_threads, want_nbest=mode == "nbest")
+            if r > 0:
+                ts.append(time.perf_counter() - t0)
+        med = float(np.median(ts))
+        return dict(threads=n_threads, utterances=len(idx), valid_frames=int(np.sum(ln)),
+                    median_s=med, mean_s=float(np.mean(ts)), frames_per_s=len(idx) * w.T / med,
+                    valid_frames_per_s=float(np.sum(ln)) / med)
+
+    one = timed(1)
+    many = timed(threads)
+    return dict(value=many["frames_per_s"], unit="frames/s", cores=many["threads"], kind="oracle",
+                sample=(f"utterances 0..{many['utterances'] - 1} of the {w.B} of the same workload "
+                        f"(one per thread; {many['valid_frames']} valid frames, T={w.T} padded), "
+                        f"one warm-up + median of {reps} runs; 1-thread figure on utterance 0"),
+                threads_1=one, threads_n=many, nproc=os.cpu_count(), usable_cores=_usable_cores(),
+                cpu_model=_cpu_model())
 
 
 def main():
@@ -122,8 +163,9 @@ def main():
     ap.add_argument("--boost-rollback", action="store_true",
                     help="end-of-utterance rollback of pending boosting")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-utts", type=int, default=8)
-    ap.add_argument("--cpu-threads", type=int, default=8)
+    ap.add_argument("--cpu-threads", type=int, default=16,
+                    help="threads (and utterances) of the multi-threaded CPU baseline, capped at "
+                         "the usable host cores")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run a plain device copy of this many MiB three times "
                          "(calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE against known bytes)")
@@ -186,7 +228,7 @@ def main():
     launch(stats)
     torch.cuda.synchronize()
     alg_bytes = algorithmic_bytes(stats.cpu().numpy(), B, T, V, 0 if mode == "greedy" else K, mode)
-    status = P.ctcbeam_query_status(ws, B)
+    status = P.ctcbeam_query_status(ws)
     for _ in range(args.warmup):
         launch()
     torch.cuda.synchronize()
@@ -225,7 +267,8 @@ def main():
                                                 ("boost_rollback", args.boost_rollback)) if on], "B": B, "T": T, "V": V, "K": 1 if mode == "greedy" else K,
                    "lm": None if w.lm is None else f"{w.lm.order}-gram, {'/'.join(str(c) for c in w.lm.counts)} explicit n-grams",
                    "boost": None if w.boost is None else f"{w.boost.n_phrases} phrases",
-                   "alpha": w.alpha, "beta": w.beta, "boost_w": w.boost_w, "theta": w.theta,
+                   "alpha": w.alpha, "beta": w.beta, "boost_w": w.boost_w,
+                   "theta": None if math.isinf(w.theta) else w.theta,
                    "parallelism": "one wave per utterance" if mode == "greedy"
                    else "one workgroup per utterance"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -248,9 +291,9 @@ def main():
         torch.cuda.synchronize()
         result["copy_calibration_bytes"] = n * 4
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, lp, lens, args.cpu_utts,
-                                              max(1, min(args.cpu_threads, os.cpu_count() or 1)), mode)
-    print(json.dumps(result), flush=True)
+        result["cpu_baseline"] = cpu_baseline(
+            w, lp, lens, max(1, min(args.cpu_threads, _usable_cores())), mode)
+    print(json.dumps(result, allow_nan=False), flush=True)
 
 
 if __name__ == "__main__":

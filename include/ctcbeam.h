@@ -124,7 +124,9 @@ int ctcbeam_boost_build_host(int vocab_size, int n_phrases, const int32_t* offse
                              const int32_t* tokens, ctcbeam_boost** out);
 void ctcbeam_boost_free(ctcbeam_boost* boost);
 
-/* Device workspace needed by a decode of this shape, in bytes. */
+/* Device workspace needed by a decode of this shape, in bytes: a 256-byte
+ * header (the batch size, for ctcbeam_query_status), a status word per
+ * utterance and the back-pointers [B, T, K] int32. */
 size_t ctcbeam_workspace_bytes(int B, int T, int K);
 
 /*
@@ -142,7 +144,8 @@ size_t ctcbeam_workspace_bytes(int B, int T, int K);
  *   lm, boost    : handles built on the current device, or NULL
  *   workspace    : device buffer of ctcbeam_workspace_bytes(B, T, K) bytes,
  *                  caller-owned, contents need no initialisation; it holds
- *                  the per-frame back-pointers and a status word per utterance
+ *                  the batch size, a status word per utterance and the
+ *                  per-frame back-pointers
  *   out_tokens   : device int32 [B, T]: best transcript, -1 padded
  *   out_lengths  : device int32 [B] (may be NULL): transcript lengths
  *   out_scores   : device fp32 [B]: best score
@@ -223,8 +226,9 @@ int ctcbeam_decode_nbest(const float* logprobs, const int32_t* lengths, int B, i
  *   logprobs, lengths, B, T, V, alpha, beta, boost_w, lm, boost, out_* :
  *                  as for ctcbeam_decode (out_lengths may be NULL)
  *   workspace    : device buffer of at least ctcbeam_workspace_bytes(B, 0, 1)
- *                  bytes (only the per-utterance status words are used; a
- *                  workspace sized for a beam decode of the same B fits)
+ *                  bytes (only the header and the per-utterance status words
+ *                  are used; a workspace sized for a beam decode of the same
+ *                  B fits)
  *   opts         : may be NULL; prune_theta and CTCBEAM_FLAG_LOGSUMEXP are
  *                  ignored (no effect with one hypothesis); stats, when given,
  *                  receives per utterance {frames, live frames, LM chain
@@ -239,10 +243,14 @@ int ctcbeam_greedy_decode(const float* logprobs, const int32_t* lengths, int B, 
                           int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
                           hipStream_t stream, const ctcbeam_opts* opts);
 
-/* Status bits of the last decode that used `workspace` (synchronises
- * `stream`): bit 0 = a length was clamped, bit 1 = internal traceback
- * mismatch, bit 2 = internal staging overflow. */
-int ctcbeam_query_status(const void* workspace, int B, hipStream_t stream, uint32_t* bits);
+/* Status bits of the last decode that used `workspace`, ORed over its
+ * utterances: bit 0 = a length was clamped, bit 1 = internal traceback
+ * mismatch, bit 2 = internal staging overflow.  Debug aid; synchronises
+ * `stream`, which must be the stream that decode was enqueued on (or one
+ * ordered after it).  The decode records its batch size in the workspace
+ * header, so the workspace alone identifies the utterances.  Returns 1 if the
+ * workspace holds no decode record (never passed to a decode). */
+int ctcbeam_query_status(const void* workspace, hipStream_t stream, uint32_t* bits);
 
 /* Thread-local message for the last non-zero return of this thread. */
 const char* ctcbeam_last_error(void);

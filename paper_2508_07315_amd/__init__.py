@@ -3,9 +3,12 @@ phrase boosting (the per-frame step of FlexCTC, arXiv 2508.07315, Algorithm 1).
 
 This module is a thin ctypes binding over the C ABI declared in
 ``include/ctcbeam.h`` and implemented by ``libctcbeam.so`` (host builders in
-``csrc/ctcbeam_host.cpp``, gfx950 kernels in ``csrc/ctcbeam_kernel.hip``).
-It only marshals arguments: every step of the search runs in the HIP kernel.
-PyTorch supplies device memory and the current stream.
+``csrc/ctcbeam_host.cpp``, gfx950 kernels in ``csrc/ctcbeam_decode.inl`` and
+``csrc/ctcbeam_greedy.inl``, compiled per vocabulary class by the
+``csrc/*.hip`` units).  It only marshals arguments: every step of the search
+runs in the HIP kernels.  PyTorch supplies device memory and streams; each
+call runs with the inputs' device current, and tensors the binding allocates
+are recorded on the launch stream when it is not torch's current stream.
 
 If the shared library has not been built, importing the binding's entry
 points raises; build it with ``python -m paper_2508_07315_amd.build_lib`` (or
@@ -85,7 +88,7 @@ def _load():
     lib.ctcbeam_greedy_decode.restype = I
     lib.ctcbeam_greedy_decode.argtypes = [P, P, I, I, I, F, F, F, P, P, P, ctypes.c_size_t, P, P, P, P, P]
     lib.ctcbeam_query_status.restype = I
-    lib.ctcbeam_query_status.argtypes = [P, I, P, ctypes.POINTER(ctypes.c_uint32)]
+    lib.ctcbeam_query_status.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32)]
     lib.ctcbeam_lm_tables.restype = I
     lib.ctcbeam_lm_tables.argtypes = [P, P]
     lib.ctcbeam_boost_tables.restype = I
@@ -109,7 +112,7 @@ FLAG_BOOST_ROLLBACK = 2   # CTCBEAM_FLAG_BOOST_ROLLBACK
 FLAG_NO_ROW_CACHE = 4     # CTCBEAM_FLAG_NO_ROW_CACHE
 
 
-def _opts(theta, stats, B, logsumexp, boost_rollback, row_cache=True):
+def _opts(theta, stats, B, logsumexp, boost_rollback, row_cache=True, device=None):
     """ctcbeam_opts by reference, or None when every option is at its default."""
     import torch
     flags = (FLAG_LOGSUMEXP if logsumexp else 0) | (FLAG_BOOST_ROLLBACK if boost_rollback else 0) | \
@@ -118,7 +121,7 @@ def _opts(theta, stats, B, logsumexp, boost_rollback, row_cache=True):
         return None
     o = _Opts()
     o.prune_theta = float(theta if theta is not None else math.inf)
-    o.stats = None if stats is None else _dptr(stats, torch.int64, "stats", (B, 8)).value
+    o.stats = None if stats is None else _dptr(stats, torch.int64, "stats", (B, 8), device).value
     o.flags = flags
     return o
 
@@ -278,12 +281,14 @@ def ctcbeam_workspace_bytes(B: int, T: int, K: int) -> int:
     return int(_load().ctcbeam_workspace_bytes(int(B), int(T), int(K)))
 
 
-def _dptr(t, dtype, name, shape=None):
+def _dptr(t, dtype, name, shape=None, device=None):
     import torch
     if t is None:
         return None
     if not isinstance(t, torch.Tensor) or not t.is_cuda:
         raise TypeError(f"{name} must be a device tensor")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the inputs on {device}")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
     if not t.is_contiguous():
@@ -293,13 +298,60 @@ def _dptr(t, dtype, name, shape=None):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _shape(logprobs):
+    if logprobs.dim() != 3:
+        raise ValueError("logprobs must be [B, T, V+1]")
+    B, T, W = (int(x) for x in logprobs.shape)
+    return B, T, W - 1, logprobs.device
+
+
+def _stream_handle(stream, dev):
+    """(raw hipStream_t, torch stream object or None) for ``stream``: None
+    (torch's current stream on dev), a torch.cuda.Stream, or a raw handle."""
+    import torch
+    if stream is None:
+        return torch.cuda.current_stream(dev).cuda_stream, None
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream, stream
+    return int(stream), None
+
+
+def _launch(call, dev, stream, owned):
+    """Run ``call(raw_stream)`` (one C entry point, returning its code) with
+    the inputs' device current.  Tensors the binding allocated (``owned``)
+    are recorded on the launch stream when it is not torch's current stream,
+    so the caching allocator does not hand their memory to other work before
+    the kernel is done with it."""
+    import torch
+    with torch.cuda.device(dev):
+        raw, obj = _stream_handle(stream, dev)
+        _check(call(ctypes.c_void_p(raw)))
+        if owned and raw != torch.cuda.current_stream(dev).cuda_stream:
+            rec = obj if obj is not None else torch.cuda.ExternalStream(raw, device=dev)
+            for t in owned:
+                t.record_stream(rec)
+
+
+def _handles(lm, boost):
+    return (lm.handle if lm is not None else None, boost.handle if boost is not None else None)
+
+
+def _alloc(t, shape, dtype, dev, owned):
+    import torch
+    if t is None:
+        t = torch.empty(shape, dtype=dtype, device=dev)
+        owned.append(t)
+    return t
+
+
 def ctcbeam_decode_ex(logprobs, lengths, K: int, alpha: float = 0.0, beta: float = 0.0,
                       boost_w: float = 0.0, lm: Optional[LM] = None,
                       boost: Optional[Boost] = None, workspace=None, out_tokens=None,
                       out_lengths=None, out_scores=None, stream=None,
                       theta: float = math.inf, stats=None, logsumexp: bool = False,
                       boost_rollback: bool = False, row_cache: bool = True):
-    """Enqueue one decode on ``stream`` (default: torch's current stream).
+    """Enqueue one decode on ``stream`` (default: torch's current stream on the
+    inputs' device; a torch.cuda.Stream or a raw hipStream_t handle).
 
     logprobs: float32 [B, T, V+1] device tensor (blank = V); lengths: int32 [B].
     Outputs are allocated when not given.  ``row_cache=False`` sets
@@ -307,33 +359,22 @@ def ctcbeam_decode_ex(logprobs, lengths, K: int, alpha: float = 0.0, beta: float
     with -1 padding, lengths [B] int32, scores [B] float32, workspace uint8)."""
     import torch
     lib = _load()
-    if logprobs.dim() != 3:
-        raise ValueError("logprobs must be [B, T, V+1]")
-    B, T, W = (int(x) for x in logprobs.shape)
-    V = W - 1
-    dev = logprobs.device
-    if out_tokens is None:
-        out_tokens = torch.empty((B, T), dtype=torch.int32, device=dev)
-    if out_lengths is None:
-        out_lengths = torch.empty((B,), dtype=torch.int32, device=dev)
-    if out_scores is None:
-        out_scores = torch.empty((B,), dtype=torch.float32, device=dev)
-    need = ctcbeam_workspace_bytes(B, T, K)
-    if workspace is None:
-        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
-    ws = _dptr(workspace, torch.uint8, "workspace")
-    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache)
-    opts = None if o is None else ctypes.byref(o)
-    if stream is None:
-        stream = torch.cuda.current_stream(dev).cuda_stream
-    rc = lib.ctcbeam_decode_ex(
-        _dptr(logprobs, torch.float32, "logprobs"), _dptr(lengths, torch.int32, "lengths", (B,)),
-        B, T, V, int(K), float(alpha), float(beta), float(boost_w),
-        lm.handle if lm is not None else None, boost.handle if boost is not None else None,
-        ws, int(workspace.numel()), _dptr(out_tokens, torch.int32, "out_tokens", (B, T)),
-        _dptr(out_lengths, torch.int32, "out_lengths", (B,)),
-        _dptr(out_scores, torch.float32, "out_scores", (B,)), ctypes.c_void_p(stream), opts)
-    _check(rc)
+    B, T, V, dev = _shape(logprobs)
+    owned = []
+    out_tokens = _alloc(out_tokens, (B, T), torch.int32, dev, owned)
+    out_lengths = _alloc(out_lengths, (B,), torch.int32, dev, owned)
+    out_scores = _alloc(out_scores, (B,), torch.float32, dev, owned)
+    workspace = _alloc(workspace, (max(ctcbeam_workspace_bytes(B, T, K), 1),), torch.uint8, dev, owned)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev)
+    args = (_dptr(logprobs, torch.float32, "logprobs", None, dev),
+            _dptr(lengths, torch.int32, "lengths", (B,), dev),
+            B, T, V, int(K), float(alpha), float(beta), float(boost_w), *_handles(lm, boost),
+            _dptr(workspace, torch.uint8, "workspace", None, dev), int(workspace.numel()),
+            _dptr(out_tokens, torch.int32, "out_tokens", (B, T), dev),
+            _dptr(out_lengths, torch.int32, "out_lengths", (B,), dev),
+            _dptr(out_scores, torch.float32, "out_scores", (B,), dev))
+    _launch(lambda st: lib.ctcbeam_decode_ex(*args, st, None if o is None else ctypes.byref(o)),
+            dev, stream, owned)
     return out_tokens, out_lengths, out_scores, workspace
 
 
@@ -352,41 +393,30 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
                          nbest_lengths=None, nbest_scores=None, stream=None,
                          theta: float = math.inf, stats=None, logsumexp: bool = False,
                          boost_rollback: bool = False, row_cache: bool = True):
-    """Enqueue one N-best decode on ``stream`` (default: torch's current stream).
+    """Enqueue one N-best decode on ``stream`` (as for ``ctcbeam_decode_ex``).
 
     Same inputs as ``ctcbeam_decode_ex``.  Returns (tokens [B,K,T] int32 with
     -1 padding, lengths [B,K] int32, scores [B,K] float32 descending,
     workspace uint8); row 0 of each utterance is the 1-best result."""
     import torch
     lib = _load()
-    if logprobs.dim() != 3:
-        raise ValueError("logprobs must be [B, T, V+1]")
-    B, T, W = (int(x) for x in logprobs.shape)
-    V = W - 1
+    B, T, V, dev = _shape(logprobs)
     K = int(K)
-    dev = logprobs.device
-    if nbest_tokens is None:
-        nbest_tokens = torch.empty((B, K, T), dtype=torch.int32, device=dev)
-    if nbest_lengths is None:
-        nbest_lengths = torch.empty((B, K), dtype=torch.int32, device=dev)
-    if nbest_scores is None:
-        nbest_scores = torch.empty((B, K), dtype=torch.float32, device=dev)
-    need = ctcbeam_workspace_bytes(B, T, K)
-    if workspace is None:
-        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
-    ws = _dptr(workspace, torch.uint8, "workspace")
-    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache)
-    opts = None if o is None else ctypes.byref(o)
-    if stream is None:
-        stream = torch.cuda.current_stream(dev).cuda_stream
-    rc = lib.ctcbeam_decode_nbest(
-        _dptr(logprobs, torch.float32, "logprobs"), _dptr(lengths, torch.int32, "lengths", (B,)),
-        B, T, V, K, float(alpha), float(beta), float(boost_w),
-        lm.handle if lm is not None else None, boost.handle if boost is not None else None,
-        ws, int(workspace.numel()), _dptr(nbest_tokens, torch.int32, "nbest_tokens", (B, K, T)),
-        _dptr(nbest_lengths, torch.int32, "nbest_lengths", (B, K)),
-        _dptr(nbest_scores, torch.float32, "nbest_scores", (B, K)), ctypes.c_void_p(stream), opts)
-    _check(rc)
+    owned = []
+    nbest_tokens = _alloc(nbest_tokens, (B, K, T), torch.int32, dev, owned)
+    nbest_lengths = _alloc(nbest_lengths, (B, K), torch.int32, dev, owned)
+    nbest_scores = _alloc(nbest_scores, (B, K), torch.float32, dev, owned)
+    workspace = _alloc(workspace, (max(ctcbeam_workspace_bytes(B, T, K), 1),), torch.uint8, dev, owned)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev)
+    args = (_dptr(logprobs, torch.float32, "logprobs", None, dev),
+            _dptr(lengths, torch.int32, "lengths", (B,), dev),
+            B, T, V, K, float(alpha), float(beta), float(boost_w), *_handles(lm, boost),
+            _dptr(workspace, torch.uint8, "workspace", None, dev), int(workspace.numel()),
+            _dptr(nbest_tokens, torch.int32, "nbest_tokens", (B, K, T), dev),
+            _dptr(nbest_lengths, torch.int32, "nbest_lengths", (B, K), dev),
+            _dptr(nbest_scores, torch.float32, "nbest_scores", (B, K), dev))
+    _launch(lambda st: lib.ctcbeam_decode_nbest(*args, st, None if o is None else ctypes.byref(o)),
+            dev, stream, owned)
     return nbest_tokens, nbest_lengths, nbest_scores, workspace
 
 
@@ -400,43 +430,35 @@ def ctcbeam_greedy_decode(logprobs, lengths, alpha: float = 0.0, beta: float = 0
     scores [B], workspace uint8)."""
     import torch
     lib = _load()
-    if logprobs.dim() != 3:
-        raise ValueError("logprobs must be [B, T, V+1]")
-    B, T, W = (int(x) for x in logprobs.shape)
-    V = W - 1
-    dev = logprobs.device
-    if out_tokens is None:
-        out_tokens = torch.empty((B, T), dtype=torch.int32, device=dev)
-    if out_lengths is None:
-        out_lengths = torch.empty((B,), dtype=torch.int32, device=dev)
-    if out_scores is None:
-        out_scores = torch.empty((B,), dtype=torch.float32, device=dev)
-    need = ctcbeam_workspace_bytes(B, 0, 1)
-    if workspace is None:
-        workspace = torch.empty((max(need, 1),), dtype=torch.uint8, device=dev)
-    ws = _dptr(workspace, torch.uint8, "workspace")
-    o = _opts(math.inf, stats, B, False, boost_rollback)
-    opts = None if o is None else ctypes.byref(o)
-    if stream is None:
-        stream = torch.cuda.current_stream(dev).cuda_stream
-    rc = lib.ctcbeam_greedy_decode(
-        _dptr(logprobs, torch.float32, "logprobs"), _dptr(lengths, torch.int32, "lengths", (B,)),
-        B, T, V, float(alpha), float(beta), float(boost_w),
-        lm.handle if lm is not None else None, boost.handle if boost is not None else None,
-        ws, int(workspace.numel()), _dptr(out_tokens, torch.int32, "out_tokens", (B, T)),
-        _dptr(out_lengths, torch.int32, "out_lengths", (B,)),
-        _dptr(out_scores, torch.float32, "out_scores", (B,)), ctypes.c_void_p(stream), opts)
-    _check(rc)
+    B, T, V, dev = _shape(logprobs)
+    owned = []
+    out_tokens = _alloc(out_tokens, (B, T), torch.int32, dev, owned)
+    out_lengths = _alloc(out_lengths, (B,), torch.int32, dev, owned)
+    out_scores = _alloc(out_scores, (B,), torch.float32, dev, owned)
+    workspace = _alloc(workspace, (max(ctcbeam_workspace_bytes(B, 0, 1), 1),), torch.uint8, dev, owned)
+    o = _opts(math.inf, stats, B, False, boost_rollback, True, dev)
+    args = (_dptr(logprobs, torch.float32, "logprobs", None, dev),
+            _dptr(lengths, torch.int32, "lengths", (B,), dev),
+            B, T, V, float(alpha), float(beta), float(boost_w), *_handles(lm, boost),
+            _dptr(workspace, torch.uint8, "workspace", None, dev), int(workspace.numel()),
+            _dptr(out_tokens, torch.int32, "out_tokens", (B, T), dev),
+            _dptr(out_lengths, torch.int32, "out_lengths", (B,), dev),
+            _dptr(out_scores, torch.float32, "out_scores", (B,), dev))
+    _launch(lambda st: lib.ctcbeam_greedy_decode(*args, st, None if o is None else ctypes.byref(o)),
+            dev, stream, owned)
     return out_tokens, out_lengths, out_scores, workspace
 
 
-def ctcbeam_query_status(workspace, B: int, stream=None) -> int:
+def ctcbeam_query_status(workspace, stream=None) -> int:
+    """Status bits (ORed over utterances) of the last decode that used
+    ``workspace``; synchronises ``stream`` (default: torch's current one)."""
     import torch
-    if stream is None:
-        stream = torch.cuda.current_stream(workspace.device).cuda_stream
+    dev = workspace.device
     bits = ctypes.c_uint32(0)
-    _check(_load().ctcbeam_query_status(ctypes.c_void_p(workspace.data_ptr()), int(B),
-                                        ctypes.c_void_p(stream), ctypes.byref(bits)))
+    with torch.cuda.device(dev):
+        raw, _ = _stream_handle(stream, dev)
+        _check(_load().ctcbeam_query_status(ctypes.c_void_p(workspace.data_ptr()),
+                                            ctypes.c_void_p(raw), ctypes.byref(bits)))
     return int(bits.value)
 
 

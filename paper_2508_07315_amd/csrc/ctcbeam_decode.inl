@@ -2186,7 +2186,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     if (wave == 0 && __ballot(bad) != 0ull) status |= 2u;
   }
   }
-  if (tid == 0) p.status[b] = status;
+  if (tid == 0) {
+    p.status[b] = status;
+    if (b == 0) write_ws_header(p.ws_header, p.B);
+  }
 }
 
 template <int LPT, int NLEV, int SPL, bool SKIP>

@@ -405,6 +405,7 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
     p.out_scores[b] = s;
     if (p.out_lengths) p.out_lengths[b] = nout;
     p.status[b] = status;
+    if (b == 0) write_ws_header(p.ws_header, p.B);
     if (p.stats) {
       int64_t* so = p.stats + static_cast<size_t>(b) * 8;
       so[0] = L;

@@ -792,7 +792,8 @@ void ctcbeam_boost_free(ctcbeam_boost* bt) {
 
 size_t ctcbeam_workspace_bytes(int B, int T, int K) {
   if (B < 0 || T < 0 || K < 0) return 0;
-  return status_bytes(B) + static_cast<size_t>(B) * static_cast<size_t>(T) * static_cast<size_t>(K) * sizeof(int32_t);
+  return ctcbeam::kWsHeaderBytes + status_bytes(B) +
+         static_cast<size_t>(B) * static_cast<size_t>(T) * static_cast<size_t>(K) * sizeof(int32_t);
 }
 
 static_assert(CTCBEAM_MAX_K == ctcbeam::kMaxK, "beam size limit");
@@ -828,7 +829,14 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
   const int flags = opts ? opts->flags : 0;
   if (flags & ~(CTCBEAM_FLAG_LOGSUMEXP | CTCBEAM_FLAG_BOOST_ROLLBACK | CTCBEAM_FLAG_NO_ROW_CACHE))
     return fail(1, "unknown flag bits");
-  if (B == 0) return 0;
+  if (B == 0) {
+    // nothing to decode; a given workspace records the empty batch
+    if (!workspace) return 0;
+    if (workspace_bytes < ctcbeam_workspace_bytes(0, 0, 0)) return fail(1, "workspace too small");
+    hipError_t e = ctcbeam::launch_ws_header(static_cast<uint32_t*>(workspace), 0, stream);
+    if (e != hipSuccess) return fail(4, std::string("kernel launch: ") + hipGetErrorString(e));
+    return 0;
+  }
   if (!lengths || !workspace || (T > 0 && !logprobs)) return fail(1, "null device pointer");
   if (want_nbest ? (!nbest_lengths || !nbest_scores || (T > 0 && !nbest_tokens))
                  : (!out_scores || (T > 0 && !out_tokens)))
@@ -863,8 +871,9 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
     p.bt_list = boost->d_list;
     p.bt_root_key = boost->d_root_key;
   }
-  p.status = static_cast<uint32_t*>(workspace);
-  p.bp = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + status_bytes(B));
+  p.ws_header = static_cast<uint32_t*>(workspace);
+  p.status = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + ctcbeam::kWsHeaderBytes);
+  p.bp = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + ctcbeam::kWsHeaderBytes + status_bytes(B));
   if (want_nbest) {
     p.nbest_tokens = nbest_tokens;  // may be null when T = 0 (empty rows)
     p.nbest_lengths = nbest_lengths;
@@ -914,12 +923,20 @@ int ctcbeam_decode(const float* logprobs, const int32_t* lengths, int B, int T, 
                            workspace_bytes, out_tokens, out_lengths, out_scores, stream, nullptr);
 }
 
-int ctcbeam_query_status(const void* workspace, int B, hipStream_t stream, uint32_t* bits) {
-  if (!workspace || !bits || B < 0) return fail(1, "null argument");
+int ctcbeam_query_status(const void* workspace, hipStream_t stream, uint32_t* bits) {
+  if (!workspace || !bits) return fail(1, "null argument");
   *bits = 0;
+  uint32_t hdr[3] = {0u, 0u, 0u};
+  hipError_t e = hipMemcpyAsync(hdr, workspace, sizeof(hdr), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return fail(4, std::string("status copy: ") + hipGetErrorString(e));
+  if (hdr[0] != ctcbeam::kWsMagic || hdr[2] != ~hdr[1] || hdr[1] > 0x7FFFFFFFu)
+    return fail(1, "workspace holds no decode record");
+  const int B = static_cast<int>(hdr[1]);
   if (B == 0) return 0;
   std::vector<uint32_t> h(B);
-  hipError_t e = hipMemcpyAsync(h.data(), workspace, sizeof(uint32_t) * B, hipMemcpyDeviceToHost, stream);
+  e = hipMemcpyAsync(h.data(), static_cast<const char*>(workspace) + ctcbeam::kWsHeaderBytes,
+                     sizeof(uint32_t) * B, hipMemcpyDeviceToHost, stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);
   if (e != hipSuccess) return fail(4, std::string("status copy: ") + hipGetErrorString(e));
   for (uint32_t v : h) *bits |= v;

@@ -16,6 +16,12 @@ constexpr uint32_t kExists = 0x80000000u;
 constexpr int kFlagLogSumExp = 1;      // recombination by log-sum-exp
 constexpr int kFlagBoostRollback = 2;  // pending boosting taken back at the end
 constexpr int kFlagNoRowCache = 4;     // LM key rows refilled for every beam every frame
+// Workspace: [header, kWsHeaderBytes][status word per utterance, padded to
+// 256 B][back-pointers [B, T, K] int32].  The header records the batch size
+// of the last decode that used the workspace, so that its status can be read
+// back from the workspace alone: {kWsMagic, B, ~B}.
+constexpr size_t kWsHeaderBytes = 256;
+constexpr uint32_t kWsMagic = 0x42435443u;  // "CTCB"
 
 // LM state record, one per chain level l (context of length l+1):
 //   {arc_begin, arc_count | kExists, backoff bits}
@@ -61,6 +67,7 @@ struct KernelParams {
   const BtEntry* bt_list;
   const uint32_t* bt_root_key;  // [V]
   // workspace / outputs
+  uint32_t* ws_header;       // workspace header (written by workgroup 0)
   uint32_t* status;          // [B]
   int32_t* bp;               // [B, T, K]
   int32_t* out_tokens;       // [B, T] or null (then no 1-best output)
@@ -75,6 +82,13 @@ struct KernelParams {
   float* nbest_scores;       // [B, K]
 };
 
+// Record the batch size in the workspace header (one thread of one workgroup).
+__device__ __forceinline__ void write_ws_header(uint32_t* hdr, int B) {
+  hdr[0] = kWsMagic;
+  hdr[1] = static_cast<uint32_t>(B);
+  hdr[2] = ~static_cast<uint32_t>(B);
+}
+
 // Kernel variants by labels per lane (V <= 512 * LPT); each dispatches on the
 // LM order and on boosting.  Return the launch's hipError_t.
 hipError_t launch_lpt1(const KernelParams& p, hipStream_t stream);
@@ -87,6 +101,9 @@ hipError_t launch_lpt8(const KernelParams& p, hipStream_t stream);
 hipError_t launch_greedy_nj4(const KernelParams& p, hipStream_t stream);
 hipError_t launch_greedy_nj16(const KernelParams& p, hipStream_t stream);
 hipError_t launch_greedy_nj64(const KernelParams& p, hipStream_t stream);
+
+// Writes the header of an empty batch (B = 0: no decode kernel runs).
+hipError_t launch_ws_header(uint32_t* hdr, int B, hipStream_t stream);
 
 inline hipError_t launch_greedy(const KernelParams& p, hipStream_t stream) {
   if (p.B == 0) return hipSuccess;

@@ -61,7 +61,7 @@ def run_gpu(lp: np.ndarray, lens: np.ndarray, K: int, alpha=0.0, beta=0.0, boost
                                           theta=theta, stats=st, stream=stream)
     torch.cuda.synchronize()
     out = dict(tokens=tok.cpu().numpy(), lengths=ln.cpu().numpy(), scores=sc.cpu().numpy(),
-               status=P.ctcbeam_query_status(ws, lp.shape[0]))
+               status=P.ctcbeam_query_status(ws))
     if stats:
         out["stats"] = st.cpu().numpy()
     return out

@@ -5,7 +5,7 @@ Bar: every row's tokens and length bit-exact, in the same order; scores
 within 1e-4 absolute (both -inf allowed).
 
 * the five workloads at reduced sizes, with and without pruning;
-* cfg3 (B=64, T=400, K=8) at full size in one launch, sampled utterances;
+* full size, every utterance of every workload: tests/test_gpu_full_size.py;
 * exhaustive pins on the GPU: with K >= (V+1)^T the live rows are exactly
   the recombination keys' best folds over all alignments;
 * row 0 equals the 1-best entry point's output; fuzzing over B, T, V, K,
@@ -43,7 +43,7 @@ def run_nbest(lp, lens, K, alpha=0.0, beta=0.0, boost_w=0.0, lm=None, boost=None
                                              theta=theta)
     torch.cuda.synchronize()
     return dict(tokens=tok.cpu().numpy(), lengths=ln.cpu().numpy(), scores=sc.cpu().numpy(),
-                status=P.ctcbeam_query_status(ws, lp.shape[0]))
+                status=P.ctcbeam_query_status(ws))
 
 
 def compare_nbest(g, r, rows=None, ref_rows=None, what=""):
@@ -91,28 +91,6 @@ def test_nbest_config_reduced(cfg):
         np.testing.assert_array_equal(g["lengths"][:, 0], one["lengths"])
         np.testing.assert_array_equal(g["scores"][:, 0], one["scores"])
         log(f"  ok, max |score diff| = {worst}")
-
-
-def test_nbest_full_size_sampled():
-    w = W.CONFIGS[3]
-    log(f"nbest cfg3 full size B={w.B} T={w.T} K={w.K}")
-    lm, bt, olm, obt = handles(w)
-    lens = W.make_lengths(w)
-    lp = W.make_logprobs(w)
-    g = run_nbest(lp, lens, w.K, w.alpha, w.beta, w.boost_w, lm, bt)
-    assert g["status"] == 0
-    smp = [0, 21, 42, 63]
-    log(f"  oracle on utterances {smp}")
-    r = _oracle(w, lp[smp], lens[smp], olm, obt)
-    compare_nbest(g, r, rows=smp, ref_rows=range(len(smp)), what="nbest cfg3 full")
-    # every utterance: rows ordered, -1 padded, dead rows last
-    for b in range(w.B):
-        sc = g["scores"][b]
-        live = int(np.sum(sc != -np.inf))
-        assert np.all(sc[:live] != -np.inf) and np.all(np.diff(sc[:live]) <= 0)
-        for k in range(w.K):
-            n = g["lengths"][b, k]
-            assert (g["tokens"][b, k, n:] == -1).all() and (g["tokens"][b, k, :n] >= 0).all()
 
 
 def _phrases(V, rng, n):

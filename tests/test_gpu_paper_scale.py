@@ -30,18 +30,3 @@ def test_six_gram_reduced(K):
                       n_threads=oracle_threads())
     compare(g, r, what=f"6-gram K={K}")
     assert g["status"] == 0
-
-
-def test_six_gram_full_size_sampled():
-    w = W.CONFIGS[6]
-    lm, bt, olm, obt = handles(w)
-    lens = W.make_lengths(w)
-    lp = W.make_logprobs(w)
-    log(f"6-gram full size B={w.B} T={w.T} K={w.K}")
-    g = run_gpu(lp, lens, w.K, w.alpha, w.beta, w.boost_w, lm, bt, theta=w.theta)
-    assert g["status"] == 0
-    smp = [int(i) for i in np.argsort(lens, kind="stable")[:2]]
-    log(f"  oracle on utterances {smp} (lengths {lens[smp].tolist()})")
-    r = oracle.decode(lp[smp], lens[smp], w.K, w.alpha, w.beta, w.boost_w, theta=w.theta,
-                      lm=olm, bt=obt, n_threads=oracle_threads())
-    compare(g, r, rows=smp, ref_rows=range(len(smp)), what="6-gram full")

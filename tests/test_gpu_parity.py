@@ -5,7 +5,7 @@ the same on both sides, so the difference is expected to be 0).
 
 * the five workloads at reduced sizes, every utterance compared, with and
   without pruning (theta = 12, the paper's setting);
-* the five workloads at full size in one launch, sampled utterances compared;
+* full size, every utterance: tests/test_gpu_full_size.py;
 * exhaustive pins on the GPU (T <= 3, V <= 3, K = 64 >= (V+1)^T);
 * fuzzing over B, T, V, K, lengths (0, T, out of range), NaN padding,
   LM order, boosting lists and theta;
@@ -52,34 +52,6 @@ def test_config_reduced(cfg):
         worst = compare(g, r, what=f"cfg{cfg} theta={th}")
         assert g["status"] == 0
         log(f"  ok, max |score diff| = {worst}")
-
-
-SAMPLES = {2: [0, 13, 31], 3: [0, 21, 42, 63], 4: "shortest2", 5: "shortest2"}
-
-
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
-def test_config_full_size_sampled(cfg):
-    import torch
-    w = W.CONFIGS[cfg]
-    log(f"cfg{cfg} full size B={w.B} T={w.T} K={w.K}: building inputs")
-    lm, bt, olm, obt = handles(w)
-    lens = W.make_lengths(w)
-    lp = W.make_logprobs(w)
-    log("  decoding on the GPU")
-    g = run_gpu(lp, lens, w.K, w.alpha, w.beta, w.boost_w, lm, bt)
-    assert g["status"] == 0
-    smp = SAMPLES.get(cfg, list(range(w.B)))
-    if smp == "shortest2":
-        smp = [int(i) for i in np.argsort(lens, kind="stable")[:2]]
-    log(f"  oracle on utterances {smp} (lengths {lens[smp].tolist()})")
-    r = _oracle(w, lp[smp], lens[smp], olm, obt)
-    worst = compare(g, r, rows=smp, ref_rows=range(len(smp)), what=f"cfg{cfg} full")
-    # every utterance: the transcript is -1 padded after its length
-    for b in range(w.B):
-        n = g["lengths"][b]
-        assert (g["tokens"][b, n:] == -1).all() and (g["tokens"][b, :n] >= 0).all()
-    log(f"  ok, max |score diff| = {worst}")
-    del torch
 
 
 def _phrases(V, rng, n):
@@ -232,3 +204,34 @@ def test_zero_lengths_and_empty_time_axis():
     g = run_gpu(lp0, np.array([0, 0]), 3, alpha=0.5, lm=lm)
     r = oracle.decode(lp0, np.array([0, 0]), 3, alpha=0.5, lm=olm)
     compare(g, r, what="T=0")
+
+
+def test_query_status_reads_the_batch_size_from_the_workspace():
+    """ctcbeam_query_status takes the workspace alone: the decode records its
+    batch size in the workspace header.  A reused workspace reports the last
+    decode (an empty batch included); a never-used one is rejected."""
+    import torch
+    dev = device()
+    rng = np.random.default_rng(4)
+    B, T, V, K = 3, 20, 9, 4
+    lp = torch.from_numpy(W.random_logprobs(rng, B, T, V)).to(dev)
+    ws = torch.zeros(P.ctcbeam_workspace_bytes(B, T, K), dtype=torch.uint8, device=dev)
+    with pytest.raises(P.CtcbeamError) as e:
+        P.ctcbeam_query_status(ws)
+    assert e.value.code == 1
+    bad = torch.tensor([-4, T + 7, 5], dtype=torch.int32, device=dev)
+    P.ctcbeam_decode_ex(lp, bad, K, beta=0.3, workspace=ws)
+    assert P.ctcbeam_query_status(ws) & 1
+    # a smaller batch in the same workspace: only its own status words count
+    ok = torch.tensor([T], dtype=torch.int32, device=dev)
+    P.ctcbeam_decode_ex(lp[2:], ok, K, beta=0.3, workspace=ws)
+    assert P.ctcbeam_query_status(ws) == 0
+    P.ctcbeam_decode_ex(lp, bad, K, beta=0.3, workspace=ws)
+    assert P.ctcbeam_query_status(ws) & 1
+    empty = torch.zeros((0, T, V + 1), dtype=torch.float32, device=dev)
+    P.ctcbeam_decode_ex(empty, torch.zeros(0, dtype=torch.int32, device=dev), K, workspace=ws)
+    assert P.ctcbeam_query_status(ws) == 0
+    # the greedy kernel records the header too
+    P.ctcbeam_greedy_decode(lp, bad, beta=0.3, workspace=ws)
+    assert P.ctcbeam_query_status(ws) & 1
+    torch.cuda.synchronize()

@@ -36,7 +36,7 @@ def _run(lp, lens, K, alpha, beta, lm, theta=math.inf, nbest=False, **kw):
     tok, ln, sc, ws = f(d_lp, d_len, K, alpha, beta, 0.0, lm, None, theta=theta, **kw)
     torch.cuda.synchronize()
     return dict(tokens=tok.cpu().numpy(), lengths=ln.cpu().numpy(), scores=sc.cpu().numpy(),
-                status=P.ctcbeam_query_status(ws, lp.shape[0]))
+                status=P.ctcbeam_query_status(ws))
 
 
 def _same(a, b, what):

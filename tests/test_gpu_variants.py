@@ -54,7 +54,7 @@ def run(lp, lens, K, alpha=0.0, beta=0.0, boost_w=0.0, lm=None, bt=None, theta=m
                                               theta=theta, **flags)
     torch.cuda.synchronize()
     return dict(tokens=tok.cpu().numpy(), lengths=ln.cpu().numpy(), scores=sc.cpu().numpy(),
-                status=P.ctcbeam_query_status(ws, lp.shape[0]))
+                status=P.ctcbeam_query_status(ws))
 
 
 def compare_nbest(g, r, what):

@@ -329,8 +329,9 @@ def test_decode_rejects_bad_arguments_before_any_device_call():
     ws = P.ctcbeam_workspace_bytes(2, 3, 4)
     dec = P._load().ctcbeam_decode_ex
 
-    def call(B=2, T=3, V=5, K=4, lm=None, bt=None, ws_bytes=ws, lp=fake, opts=None, alpha=0.0):
-        return dec(lp, fake, B, T, V, K, alpha, 0.0, 0.0, lm, bt, fake, ws_bytes, fake, null, fake,
+    def call(B=2, T=3, V=5, K=4, lm=None, bt=None, ws_bytes=ws, lp=fake, opts=None, alpha=0.0,
+             wsp=fake):
+        return dec(lp, fake, B, T, V, K, alpha, 0.0, 0.0, lm, bt, wsp, ws_bytes, fake, null, fake,
                    null, opts)
 
     assert call(K=0) == 1
@@ -342,7 +343,9 @@ def test_decode_rejects_bad_arguments_before_any_device_call():
     assert call(ws_bytes=ws - 1) == 1
     assert call(lp=null) == 1
     assert call(alpha=float("nan")) == 1
-    assert call(B=0) == 0  # nothing to do, nothing launched
+    # B = 0 without a workspace: nothing to do, nothing launched (with one,
+    # a one-thread kernel records the empty batch in its header)
+    assert call(B=0, wsp=null) == 0
     rng = np.random.default_rng(0)
     lm = P.ctcbeam_lm_build_host(W.random_small_lm(rng, 2, 5))
     assert call(lm=lm.handle) == 1            # host-only handle
@@ -360,5 +363,20 @@ def test_workspace_bytes_formula():
     for B, T, K in [(1, 1, 1), (64, 400, 8), (128, 1000, 16), (3, 0, 5)]:
         n = P.ctcbeam_workspace_bytes(B, T, K)
         assert n >= B * T * K * 4 + B * 4
-        assert n - B * T * K * 4 <= 4 * B + 256
-    assert math.isfinite(P.ctcbeam_workspace_bytes(0, 0, 1))
+        assert n - B * T * K * 4 <= 4 * B + 256 + 256  # status words + header
+    assert P.ctcbeam_workspace_bytes(0, 0, 1) == 256  # the header alone
+
+
+def test_query_status_signature_matches_the_boundary():
+    """ctcbeam_query_status(const void* workspace, hipStream_t stream,
+    uint32_t* bits): the batch size comes from the workspace header."""
+    hdr = open(os.path.join(ROOT, "include", "ctcbeam.h")).read()
+    m = re.search(r"int\s+ctcbeam_query_status\s*\(([^)]*)\)", hdr)
+    assert m, "ctcbeam_query_status is not declared"
+    params = [" ".join(a.split()) for a in m.group(1).split(",")]
+    assert params == ["const void* workspace", "hipStream_t stream", "uint32_t* bits"], params
+    lib = P._load()
+    assert len(lib.ctcbeam_query_status.argtypes) == 3
+    # no device call is made for a null workspace
+    bits = ctypes.c_uint32(7)
+    assert lib.ctcbeam_query_status(None, None, ctypes.byref(bits)) == 1
