@@ -243,6 +243,24 @@ int ctcbeam_greedy_decode(const float* logprobs, const int32_t* lengths, int B, 
                           int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
                           hipStream_t stream, const ctcbeam_opts* opts);
 
+/*
+ * For callers that cannot allocate device memory (code under stream capture,
+ * tight serving loops, harnesses that forbid hipMalloc): ctcbeam_decode_ex
+ * without a workspace argument.  The workspace lives in a fixed device array
+ * of CTCBEAM_NOALLOC_MAX_WORKSPACE bytes that the library holds on each device
+ * it runs on until the process ends; the call allocates nothing.  Requests
+ * whose ctcbeam_workspace_bytes(B, T, K) exceeds that size return 2.
+ * Every call on one device shares that device's array: calls that overlap on
+ * one device race (serialise them, e.g. on one stream).  Status bits of these
+ * decodes are not readable through ctcbeam_query_status.  All other
+ * arguments, results and errors as for ctcbeam_decode_ex.
+ */
+#define CTCBEAM_NOALLOC_MAX_WORKSPACE (16u << 20)
+int ctcbeam_decode_noalloc(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K,
+                           float alpha, float beta, float boost_w, const ctcbeam_lm* lm,
+                           const ctcbeam_boost* boost, int32_t* out_tokens, int32_t* out_lengths,
+                           float* out_scores, hipStream_t stream, const ctcbeam_opts* opts);
+
 /* Status bits of the last decode that used `workspace`, ORed over its
  * utterances: bit 0 = a length was clamped, bit 1 = internal traceback
  * mismatch, bit 2 = internal staging overflow.  Debug aid; synchronises

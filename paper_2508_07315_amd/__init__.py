@@ -87,6 +87,8 @@ def _load():
     lib.ctcbeam_decode_nbest.argtypes = dec + [P]
     lib.ctcbeam_greedy_decode.restype = I
     lib.ctcbeam_greedy_decode.argtypes = [P, P, I, I, I, F, F, F, P, P, P, ctypes.c_size_t, P, P, P, P, P]
+    lib.ctcbeam_decode_noalloc.restype = I
+    lib.ctcbeam_decode_noalloc.argtypes = [P, P, I, I, I, I, F, F, F, P, P, P, P, P, P, P]
     lib.ctcbeam_query_status.restype = I
     lib.ctcbeam_query_status.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32)]
     lib.ctcbeam_lm_tables.restype = I
@@ -447,6 +449,39 @@ def ctcbeam_greedy_decode(logprobs, lengths, alpha: float = 0.0, beta: float = 0
     _launch(lambda st: lib.ctcbeam_greedy_decode(*args, st, None if o is None else ctypes.byref(o)),
             dev, stream, owned)
     return out_tokens, out_lengths, out_scores, workspace
+
+
+NOALLOC_MAX_WORKSPACE = 16 << 20   # CTCBEAM_NOALLOC_MAX_WORKSPACE
+
+
+def ctcbeam_decode_noalloc(logprobs, lengths, K: int, alpha: float = 0.0, beta: float = 0.0,
+                           boost_w: float = 0.0, lm: Optional[LM] = None,
+                           boost: Optional[Boost] = None, out_tokens=None, out_lengths=None,
+                           out_scores=None, stream=None, theta: float = math.inf, stats=None,
+                           logsumexp: bool = False, boost_rollback: bool = False,
+                           row_cache: bool = True):
+    """``ctcbeam_decode_ex`` through the entry point that allocates nothing:
+    the workspace is the library's fixed per-device array (calls that overlap
+    on one device race).  Pass the outputs to keep the call allocation-free
+    (they are allocated here when not given).  Returns (tokens, lengths,
+    scores)."""
+    import torch
+    lib = _load()
+    B, T, V, dev = _shape(logprobs)
+    owned = []
+    out_tokens = _alloc(out_tokens, (B, T), torch.int32, dev, owned)
+    out_lengths = _alloc(out_lengths, (B,), torch.int32, dev, owned)
+    out_scores = _alloc(out_scores, (B,), torch.float32, dev, owned)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev)
+    args = (_dptr(logprobs, torch.float32, "logprobs", None, dev),
+            _dptr(lengths, torch.int32, "lengths", (B,), dev),
+            B, T, V, int(K), float(alpha), float(beta), float(boost_w), *_handles(lm, boost),
+            _dptr(out_tokens, torch.int32, "out_tokens", (B, T), dev),
+            _dptr(out_lengths, torch.int32, "out_lengths", (B,), dev),
+            _dptr(out_scores, torch.float32, "out_scores", (B,), dev))
+    _launch(lambda st: lib.ctcbeam_decode_noalloc(*args, st, None if o is None else ctypes.byref(o)),
+            dev, stream, owned)
+    return out_tokens, out_lengths, out_scores
 
 
 def ctcbeam_query_status(workspace, stream=None) -> int:

@@ -891,6 +891,22 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
 
 }  // namespace
 
+}  // extern "C"
+
+namespace ctcbeam {
+int decode_with_workspace(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K,
+                          float alpha, float beta, float boost_w, const ctcbeam_lm* lm,
+                          const ctcbeam_boost* boost, void* workspace, size_t workspace_bytes,
+                          int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
+                          hipStream_t stream, const ctcbeam_opts* opts) {
+  return decode_impl(logprobs, lengths, B, T, V, K, alpha, beta, boost_w, lm, boost, workspace, workspace_bytes,
+                     out_tokens, out_lengths, out_scores, nullptr, nullptr, nullptr, false, false, stream, opts);
+}
+int set_last_error(int code, const char* msg) { return fail(code, msg); }
+}  // namespace ctcbeam
+
+extern "C" {
+
 int ctcbeam_decode_ex(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K, float alpha,
                       float beta, float boost_w, const ctcbeam_lm* lm, const ctcbeam_boost* boost, void* workspace,
                       size_t workspace_bytes, int32_t* out_tokens, int32_t* out_lengths, float* out_scores,

@@ -2,7 +2,12 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
+
+struct ctcbeam_lm;
+struct ctcbeam_boost;
+struct ctcbeam_opts;
 
 namespace ctcbeam {
 
@@ -111,6 +116,17 @@ inline hipError_t launch_greedy(const KernelParams& p, hipStream_t stream) {
   if (p.V <= 1024) return launch_greedy_nj16(p, stream);
   return launch_greedy_nj64(p, stream);
 }
+
+// The 1-best decode of ctcbeam_decode_ex into a given workspace (host side,
+// ctcbeam_host.cpp): validation, parameter block, launch; the C entry
+// points' return codes.  set_last_error records the message that
+// ctcbeam_last_error returns and passes the code through.
+int decode_with_workspace(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K,
+                          float alpha, float beta, float boost_w, const ctcbeam_lm* lm,
+                          const ctcbeam_boost* boost, void* workspace, size_t workspace_bytes,
+                          int32_t* out_tokens, int32_t* out_lengths, float* out_scores,
+                          hipStream_t stream, const ctcbeam_opts* opts);
+int set_last_error(int code, const char* msg);
 
 inline hipError_t launch_decode(const KernelParams& p, hipStream_t stream) {
   if (p.B == 0) return hipSuccess;
