@@ -864,6 +864,7 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
     p.lm_unigram = lm->d_unigram;
     p.lm_nlev = lm->nlev;
     p.lm_states_below_2p23 = lm->n_states <= (int64_t(1) << 23) ? 1 : 0;
+    p.lm_n_states = lm->n_states;
     p.lm_bos_state = static_cast<uint32_t>(V);
   }
   if (boost) {

@@ -67,6 +67,7 @@ struct KernelParams {
   int lm_nlev;
   uint32_t lm_bos_state;
   int lm_states_below_2p23;  // every LM state id fits 23 bits
+  int64_t lm_n_states;       // number of LM states
   // boosting (null when disabled)
   const BtNode* bt_nodes;
   const BtEntry* bt_list;
@@ -128,8 +129,15 @@ int decode_with_workspace(const float* logprobs, const int32_t* lengths, int B, 
                           hipStream_t stream, const ctcbeam_opts* opts);
 int set_last_error(int code, const char* msg);
 
+// Small-beam decoder (ctcbeam_small.inl): beams of at most 8, at most 1024
+// tokens, an n-gram LM of 1..7 backoff levels or none, no boosting, max
+// recombination, LM rows kept across frames.
+bool small_beam_eligible(const KernelParams& p);
+hipError_t launch_small(const KernelParams& p, hipStream_t stream);
+
 inline hipError_t launch_decode(const KernelParams& p, hipStream_t stream) {
   if (p.B == 0) return hipSuccess;
+  if (small_beam_eligible(p)) return launch_small(p, stream);
   if (p.V <= 512) return launch_lpt1(p, stream);
   if (p.V <= 1024) return launch_lpt2(p, stream);
   if (p.V <= 2048) return launch_lpt4(p, stream);
