@@ -172,7 +172,8 @@ def decode(logprobs: np.ndarray, lengths, K: int, alpha: float = 0.0, beta: floa
            boost_w: float = 0.0, theta: float = math.inf, lm: Optional[LM] = None,
            bt: Optional[BT] = None, n_threads: int = 1, want_align: bool = False,
            want_trace: bool = False, want_counters: bool = False, want_nbest: bool = False,
-           logsumexp: bool = False, boost_rollback: bool = False) -> dict:
+           logsumexp: bool = False, boost_rollback: bool = False,
+           repeat_score: bool = False) -> dict:
     """Run the oracle on host arrays.  logprobs: fp32 [B, T, V+1] (blank = V).
 
     want_nbest adds every slot's final hypothesis ordered by final score
@@ -180,9 +181,10 @@ def decode(logprobs: np.ndarray, lengths, K: int, alpha: float = 0.0, beta: floa
     [B, K, T] (-1 padded), nbest_lengths [B, K], nbest_scores [B, K].
     logsumexp merges recombined hypotheses with lse32 instead of max;
     boost_rollback takes back the pending boosting of unfinished phrases at
-    the end of the utterance."""
+    the end of the utterance; repeat_score adds the LM and boosting terms of
+    a token again at every frame that repeats it."""
     lib = _load()
-    flags = (1 if logsumexp else 0) | (2 if boost_rollback else 0)
+    flags = (1 if logsumexp else 0) | (2 if boost_rollback else 0) | (4 if repeat_score else 0)
     lp = np.ascontiguousarray(logprobs, dtype=np.float32)
     B, T, W = lp.shape
     V = W - 1

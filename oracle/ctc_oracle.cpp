@@ -32,7 +32,13 @@
 //     takes lse32(own, other) for each later duplicate in slot order, which
 //     sums the probability of all alignments of a transcript; bit 1 rolls
 //     back the pending boosting of an unfinished phrase at the end of the
-//     utterance: after LM.Final, alive scores get fl(w * -pot(q));
+//     utterance: after LM.Final, alive scores get fl(w * -pot(q)); bit 2
+//     scores repeated emissions with the LM and boosting at every
+//     occurrence (Sec. III-C mentions this as a tried alternative): a frame
+//     that repeats the beam's last frame label (a token) adds again the
+//     fl(alpha * LM) and fl(w * BT) terms that the token received when it was
+//     emitted, x = ((s + D[c]) + al) + wb, with no beta and no state change
+//     (the LM and boosting states advance once per token of the transcript);
 //   * output: best slot, lowest index on ties; if its score is -inf the
 //     transcript is empty and the score -inf;
 //   * N-best output (all K final hypotheses, the batched-hypotheses result of
@@ -195,6 +201,8 @@ struct OracleBT {
 struct Hyp {
   float s = NEG_INF;
   int32_t last = 0;
+  float rep_al = 0.0f;      // fl(alpha * LM) and fl(w * BT) received by the
+  float rep_wb = 0.0f;      // last emitted token (repeat-scoring variant)
   std::vector<int32_t> y;   // collapsed transcript
   std::vector<int32_t> q;   // boosting-tree state (node string)
 };
@@ -262,6 +270,7 @@ float lse32(float a, float b) {
 
 constexpr int kFlagLogSumExp = 1;
 constexpr int kFlagBoostRollback = 2;
+constexpr int kFlagRepeatScore = 4;
 
 struct DecodeArgs {
   const float* logprobs;
@@ -315,6 +324,11 @@ void decode_one(const DecodeArgs& a, int b) {
       for (int c = 0; c < W; ++c) {
         float x = h.s + D[c];
         bool emit = (c != V) && (c != h.last);
+        const bool rep = (a.flags & kFlagRepeatScore) && c != V && c == h.last;
+        if (rep && alive) {
+          if (a.lm) x = x + h.rep_al;
+          if (a.bt) x = x + h.rep_wb;
+        }
         if (emit && alive) {
           x = x + a.beta;
           if (a.lm) {
@@ -354,10 +368,14 @@ void decode_one(const DecodeArgs& a, int b) {
       n.last = c;
       n.y = ph.y;
       n.q = ph.q;
+      n.rep_al = ph.rep_al;
+      n.rep_wb = ph.rep_wb;
       if (emit) {
+        if (a.lm) n.rep_al = a.alpha * a.lm->score(ph.y, c);
         n.y.push_back(c);
         if (a.bt) {
-          a.bt->step(ph.q, c, &tmp);
+          const int sc = a.bt->step(ph.q, c, &tmp);
+          n.rep_wb = a.boost_w * static_cast<float>(sc);
           n.q = tmp;
         }
         if (x != NEG_INF) cnt[6] += 1;
@@ -556,7 +574,8 @@ float oracle_lse32(float a, float b) { return lse32(a, b); }
 // over std::threads.  Optional outputs (null to skip): the best path's frame
 // labels, per-frame back-pointer indices and slot scores, work counters, and
 // the N-best list (tokens [B,K,T], lengths [B,K], scores [B,K]).  flags: bit 0
-// log-sum-exp recombination, bit 1 end-of-utterance boosting rollback.
+// log-sum-exp recombination, bit 1 end-of-utterance boosting rollback, bit 2
+// LM / boosting scores of repeated emissions.
 // Returns 0 on success, 1 on invalid arguments.
 int oracle_decode(const float* logprobs, const int32_t* lengths, int B, int T, int V, int K,
                   float alpha, float beta, float boost_w, float theta, int flags, const void* lm,

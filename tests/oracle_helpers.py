@@ -27,27 +27,38 @@ def collapse(align, V):
 
 
 def fold_alignment(D, align, V, alpha=0.0, beta=0.0, boost_w=0.0, lm=None, bt=None,
-                   rollback=False):
+                   rollback=False, repeat=False):
     """fp32 score of one alignment: the per-frame left fold of the candidate
     score (Alg. 1 score update, Eq. 1), then LM.Final (and, with rollback, the
-    pending boosting taken back).  D: [T, V+1] fp32."""
+    pending boosting taken back).  With repeat, a frame that repeats the
+    previous frame's token adds that token's LM and boosting terms again
+    (the terms it got when it was emitted; no beta).  D: [T, V+1] fp32."""
     s = F32(0.0)
     last = V
     y = []
     q = []
+    terms = []  # the LM and boosting terms of the last emitted token
     for t, c in enumerate(align):
         c = int(c)
         x = F32(s + F32(D[t, c]))
         emit = c != V and c != last
         if emit:
             x = F32(x + F32(beta))
+            terms = []
             if lm is not None:
-                x = F32(x + F32(F32(alpha) * F32(lm.score(y, c))))
+                al = F32(F32(alpha) * F32(lm.score(y, c)))
+                x = F32(x + al)
+                terms.append(al)
             if bt is not None:
                 sc, q2 = bt.step(q, c)
-                x = F32(x + F32(F32(boost_w) * F32(sc)))
+                wb = F32(F32(boost_w) * F32(sc))
+                x = F32(x + wb)
+                terms.append(wb)
                 q = q2
             y.append(c)
+        elif repeat and c != V:
+            for v in terms:
+                x = F32(x + v)
         last = c
         s = x
     if lm is not None:
