@@ -178,6 +178,15 @@ int ctcbeam_decode(const float* logprobs, const int32_t* lengths, int B, int T, 
                                           V of 513..1024 with K <= 8, up to
                                           2048 with K <= 4, up to 4096 with
                                           K <= 2) */
+#define CTCBEAM_FLAG_REPEAT_SCORE 8    /* Sec. III-C's alternative of scoring
+                                          repeated emissions at every
+                                          occurrence: a frame that repeats the
+                                          beam's last frame label (a token)
+                                          adds again the fl(alpha * LM) and
+                                          fl(boost_w * BT) terms that token got
+                                          when it was emitted (no beta; the LM
+                                          and boosting states do not move).
+                                          Beam, N-best and greedy paths. */
 
 typedef struct ctcbeam_opts {
   float prune_theta;   /* Algorithm 1 threshold theta; +inf disables pruning */

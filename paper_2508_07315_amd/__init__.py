@@ -112,13 +112,15 @@ class _Opts(ctypes.Structure):
 FLAG_LOGSUMEXP = 1        # CTCBEAM_FLAG_LOGSUMEXP
 FLAG_BOOST_ROLLBACK = 2   # CTCBEAM_FLAG_BOOST_ROLLBACK
 FLAG_NO_ROW_CACHE = 4     # CTCBEAM_FLAG_NO_ROW_CACHE
+FLAG_REPEAT_SCORE = 8     # CTCBEAM_FLAG_REPEAT_SCORE
 
 
-def _opts(theta, stats, B, logsumexp, boost_rollback, row_cache=True, device=None):
+def _opts(theta, stats, B, logsumexp, boost_rollback, row_cache=True, device=None,
+          repeat_score=False):
     """ctcbeam_opts by reference, or None when every option is at its default."""
     import torch
     flags = (FLAG_LOGSUMEXP if logsumexp else 0) | (FLAG_BOOST_ROLLBACK if boost_rollback else 0) | \
-        (0 if row_cache else FLAG_NO_ROW_CACHE)
+        (0 if row_cache else FLAG_NO_ROW_CACHE) | (FLAG_REPEAT_SCORE if repeat_score else 0)
     if (theta is None or math.isinf(theta)) and stats is None and flags == 0:
         return None
     o = _Opts()
@@ -351,13 +353,15 @@ def ctcbeam_decode_ex(logprobs, lengths, K: int, alpha: float = 0.0, beta: float
                       boost: Optional[Boost] = None, workspace=None, out_tokens=None,
                       out_lengths=None, out_scores=None, stream=None,
                       theta: float = math.inf, stats=None, logsumexp: bool = False,
-                      boost_rollback: bool = False, row_cache: bool = True):
+                      boost_rollback: bool = False, row_cache: bool = True,
+                      repeat_score: bool = False):
     """Enqueue one decode on ``stream`` (default: torch's current stream on the
     inputs' device; a torch.cuda.Stream or a raw hipStream_t handle).
 
     logprobs: float32 [B, T, V+1] device tensor (blank = V); lengths: int32 [B].
     Outputs are allocated when not given.  ``row_cache=False`` sets
-    CTCBEAM_FLAG_NO_ROW_CACHE (same results).  Returns (tokens [B,T] int32
+    CTCBEAM_FLAG_NO_ROW_CACHE (same results); ``repeat_score=True`` sets
+    CTCBEAM_FLAG_REPEAT_SCORE.  Returns (tokens [B,T] int32
     with -1 padding, lengths [B] int32, scores [B] float32, workspace uint8)."""
     import torch
     lib = _load()
@@ -367,7 +371,7 @@ def ctcbeam_decode_ex(logprobs, lengths, K: int, alpha: float = 0.0, beta: float
     out_lengths = _alloc(out_lengths, (B,), torch.int32, dev, owned)
     out_scores = _alloc(out_scores, (B,), torch.float32, dev, owned)
     workspace = _alloc(workspace, (max(ctcbeam_workspace_bytes(B, T, K), 1),), torch.uint8, dev, owned)
-    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev, repeat_score)
     args = (_dptr(logprobs, torch.float32, "logprobs", None, dev),
             _dptr(lengths, torch.int32, "lengths", (B,), dev),
             B, T, V, int(K), float(alpha), float(beta), float(boost_w), *_handles(lm, boost),
@@ -394,7 +398,8 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
                          boost: Optional[Boost] = None, workspace=None, nbest_tokens=None,
                          nbest_lengths=None, nbest_scores=None, stream=None,
                          theta: float = math.inf, stats=None, logsumexp: bool = False,
-                         boost_rollback: bool = False, row_cache: bool = True):
+                         boost_rollback: bool = False, row_cache: bool = True,
+                         repeat_score: bool = False):
     """Enqueue one N-best decode on ``stream`` (as for ``ctcbeam_decode_ex``).
 
     Same inputs as ``ctcbeam_decode_ex``.  Returns (tokens [B,K,T] int32 with
@@ -409,7 +414,7 @@ def ctcbeam_decode_nbest(logprobs, lengths, K: int, alpha: float = 0.0, beta: fl
     nbest_lengths = _alloc(nbest_lengths, (B, K), torch.int32, dev, owned)
     nbest_scores = _alloc(nbest_scores, (B, K), torch.float32, dev, owned)
     workspace = _alloc(workspace, (max(ctcbeam_workspace_bytes(B, T, K), 1),), torch.uint8, dev, owned)
-    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev, repeat_score)
     args = (_dptr(logprobs, torch.float32, "logprobs", None, dev),
             _dptr(lengths, torch.int32, "lengths", (B,), dev),
             B, T, V, K, float(alpha), float(beta), float(boost_w), *_handles(lm, boost),
@@ -426,7 +431,7 @@ def ctcbeam_greedy_decode(logprobs, lengths, alpha: float = 0.0, beta: float = 0
                           boost_w: float = 0.0, lm: Optional[LM] = None,
                           boost: Optional[Boost] = None, workspace=None, out_tokens=None,
                           out_lengths=None, out_scores=None, stream=None, stats=None,
-                          boost_rollback: bool = False):
+                          boost_rollback: bool = False, repeat_score: bool = False):
     """Enqueue one greedy decode with fusion (Algorithm 1 with one hypothesis)
     on ``stream``.  Returns (tokens [B,T] int32 with -1 padding, lengths [B],
     scores [B], workspace uint8)."""
@@ -438,7 +443,7 @@ def ctcbeam_greedy_decode(logprobs, lengths, alpha: float = 0.0, beta: float = 0
     out_lengths = _alloc(out_lengths, (B,), torch.int32, dev, owned)
     out_scores = _alloc(out_scores, (B,), torch.float32, dev, owned)
     workspace = _alloc(workspace, (max(ctcbeam_workspace_bytes(B, 0, 1), 1),), torch.uint8, dev, owned)
-    o = _opts(math.inf, stats, B, False, boost_rollback, True, dev)
+    o = _opts(math.inf, stats, B, False, boost_rollback, True, dev, repeat_score)
     args = (_dptr(logprobs, torch.float32, "logprobs", None, dev),
             _dptr(lengths, torch.int32, "lengths", (B,), dev),
             B, T, V, float(alpha), float(beta), float(boost_w), *_handles(lm, boost),
@@ -459,7 +464,7 @@ def ctcbeam_decode_noalloc(logprobs, lengths, K: int, alpha: float = 0.0, beta: 
                            boost: Optional[Boost] = None, out_tokens=None, out_lengths=None,
                            out_scores=None, stream=None, theta: float = math.inf, stats=None,
                            logsumexp: bool = False, boost_rollback: bool = False,
-                           row_cache: bool = True):
+                           row_cache: bool = True, repeat_score: bool = False):
     """``ctcbeam_decode_ex`` through the entry point that allocates nothing:
     the workspace is the library's fixed per-device array (calls that overlap
     on one device race).  Pass the outputs to keep the call allocation-free
@@ -472,7 +477,7 @@ def ctcbeam_decode_noalloc(logprobs, lengths, K: int, alpha: float = 0.0, beta: 
     out_tokens = _alloc(out_tokens, (B, T), torch.int32, dev, owned)
     out_lengths = _alloc(out_lengths, (B,), torch.int32, dev, owned)
     out_scores = _alloc(out_scores, (B,), torch.float32, dev, owned)
-    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev)
+    o = _opts(theta, stats, B, logsumexp, boost_rollback, row_cache, dev, repeat_score)
     args = (_dptr(logprobs, torch.float32, "logprobs", None, dev),
             _dptr(lengths, torch.int32, "lengths", (B,), dev),
             B, T, V, int(K), float(alpha), float(beta), float(boost_w), *_handles(lm, boost),

@@ -169,7 +169,9 @@ __device__ __forceinline__ bool dup_by_sort(uint64_t key, int lane, uint32_t& lo
 // CACHE (one chunk, one slot per lane, LM without boosting, LM states below
 // 2^23): LM key rows are kept per LM state across frames and only the states
 // new to the rows are filled; an entry holds its arc's target state.
-template <int LPT, int NLEV, bool HAS_BT, int SPL, bool SKIP, bool CACHE>
+// REP: the repeat-scoring variant (CTCBEAM_FLAG_REPEAT_SCORE), a kernel of
+// its own so that the default kernels carry none of its state.
+template <int LPT, int NLEV, bool HAS_BT, int SPL, bool SKIP, bool CACHE, bool REP>
 __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool HAS_LM = NLEV >= 0;
   constexpr int NL = NLEV > 0 ? NLEV : 0;     // chain levels above the unigram root
@@ -210,13 +212,16 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // back-pointer, transcript hash (2), length, last label, LM state, then
   // with boosting: boosting state, emitted flag, boosting list
   // begin/count/pot; without: emitted flag; then LM chain begin[NL],
-  // count[NL], backoff[NL].  The boosting fields exist (and are accessed)
-  // only with boosting.
+  // count[NL], backoff[NL]; then the fl(alpha*LM) and fl(w*BT) terms the
+  // last emitted token received (read by the repeat-scoring variant).  The
+  // boosting fields exist (and are accessed) only with boosting.
   constexpr int kRX = 0, kRBp = 1, kRHlo = 2, kRHhi = 3, kRLen = 4, kRLast = 5, kRLms = 6;
   constexpr int kRBts = 7, kRBtb = 9, kRBtc = 10, kRBtp = 11;
   constexpr int kREmit = HAS_BT ? 8 : 7;
   constexpr int kRLvb = HAS_BT ? 12 : 8, kRLvc = kRLvb + NL, kRLvbo = kRLvb + 2 * NL;
-  constexpr int RW = (kRLvb + 3 * NL + 3) & ~3;
+  constexpr int kRRal = kRLvb + 3 * NL, kRRwb = kRRal + 1;
+  constexpr int RW = ((REP ? kRRwb + 1 : kRRal) + 3) & ~3;
+  static_assert(!(REP && CACHE), "the repeat-scoring variant reads uncached rows");
 
   __shared__ __align__(16) uint32_t s_big[kBigWords];
   // survivor pool: score bits, flat index, LM target (raw), boosting key
@@ -224,6 +229,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   static_assert(kCap / 2 <= kThreads, "the fallback reads carried pool entries one per thread");
   // reserved regions (ping-pong): blank candidates, or the best K so far
   __shared__ uint4 s_res[2][KMX];
+  // repeat-scoring variant only: the (fl(alpha*LM), fl(w*BT)) terms of the
+  // pool entries and of the reserved entries, moved along with them
+  __shared__ float2 s_pinc[REP ? kCap : 1];
+  __shared__ float2 s_rinc[2][REP ? KMX : 1];
   // beam records by live position: score, last label, slot (and key row),
   // boosting pot, backoff weights unless the rows hold the fold; reused by
   // the epilogue (lengths and ranks, 2 KMX words)
@@ -260,6 +269,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   const int kcmax = min(K, KSEG);
   const float alpha = p.alpha, beta = p.beta, boost_w = p.boost_w;
   const uint64_t lmlt = lanemask_lt();
+  // repeat-scoring variant: a repeated token gets its LM / boosting terms again
+  constexpr bool rep = REP;
 
   int L = p.lengths[b];
   uint32_t status = 0;
@@ -376,6 +387,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 #pragma unroll
     for (int w4 = 0; w4 < RW; w4 += 4) *reinterpret_cast<uint4*>(dst + w4) = make_uint4(r[w4], r[w4 + 1], r[w4 + 2], r[w4 + 3]);
   };
+  // repeat-scoring variant: the terms of an emitted token into its record
+  auto put_terms = [&](uint32_t* dst, float2 inc) __attribute__((always_inline)) {
+    dst[kRRal] = __float_as_uint(inc.x);
+    dst[kRRwb] = __float_as_uint(inc.y);
+  };
   // Successor of a selected candidate (flat index idx, resolved LM target,
   // boosting key) from its parent's record.  succ_begin reads the parent and
   // starts the chain-header loads of an emitted token; succ_end builds the
@@ -432,6 +448,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 
   for (int i = tid; i < kOffTgt; i += kThreads) s_big[i] = 0u;
   for (int i = tid; i < (KMX + 16) * kRowWords; i += kThreads) s_row[i] = 0u;
+  if constexpr (REP)
+    for (int i = tid; i < 2 * KMX; i += kThreads) s_rinc[i / KMX][i % KMX] = make_float2(0.0f, 0.0f);
   __syncthreads();
   if (tid == 0) {
     put_row(0, 0);
@@ -818,6 +836,77 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         }
         lmax = fmaxf(lmax, rmax[i]);
       }
+      if constexpr (rep) {
+        // repeat-scoring variant: the repeat of a live row's last label (a
+        // token) adds the terms that token got when it was emitted, read
+        // from the slot's record; the maxima are taken again
+        const uint32_t* prc = s_rec + rcur * (KMX * RW);
+        lmax = kNegInf;
+#pragma unroll
+        for (int i = 0; i < KCR; ++i) {
+          const uint32_t* rr = prc + (static_cast<uint32_t>(kslot[i]) & (KMX - 1)) * RW;
+          const float ral = __uint_as_float(rr[kRRal]), rwb = __uint_as_float(rr[kRRwb]);
+#pragma unroll
+          for (int jj = 0; jj < LPT; ++jj) {
+            const int r = i * LPT + jj;
+            const int c = tid + jj * kThreads;
+            if (i < kc && c < V && c == klast[i]) {
+              float x = cand[r];
+              if (HAS_LM) x = x + ral;
+              if (HAS_BT) x = x + rwb;
+              cand[r] = x;
+            }
+            rmax[i] = jj == 0 ? cand[r] : fmaxf(rmax[i], cand[r]);
+          }
+          lmax = fmaxf(lmax, rmax[i]);
+        }
+      }
+      // The (fl(alpha*LM), fl(w*BT)) terms of candidate (chunk row i, label
+      // c) as the scoring formed them, from this chunk's rows, for the
+      // repeat-scoring variant (run-time i and c; kc rows of the chunk).
+      const auto cand_terms = [&](uint32_t i, uint32_t c, uint32_t row) __attribute__((always_inline)) {
+        float av = 0.0f, bv = 0.0f;
+        const uint32_t e = i * static_cast<uint32_t>(V) + c;
+        const uint32_t* rr = s_row + (static_cast<uint32_t>(cs) + i) * kRowWords;
+        if (HAS_LM) {
+          if constexpr (CACHE) {
+            av = __uint_as_float(static_cast<uint32_t>(lmrow[row * static_cast<uint32_t>(V) + c]));
+          } else if constexpr (kFoldRows) {
+            av = __uint_as_float(static_cast<uint32_t>(lmrow[e]));
+          } else {
+            const uint64_t ent = lmrow[e];
+            if (static_cast<uint32_t>(ent >> 32) >= genhi) {
+              av = __uint_as_float(static_cast<uint32_t>(ent));
+            } else {
+              float v = p.lm_unigram[c];
+#pragma unroll
+              for (int l = 0; l < NL; ++l) v = v + __uint_as_float(rr[4 + l]);
+              av = alpha * v;
+            }
+          }
+        }
+        if (HAS_BT) {
+          const uint32_t be = btrow[e];
+          const uint32_t bk = (be >= genhi) ? be : p.bt_root_key[c];
+          bv = boost_w * static_cast<float>(static_cast<int>((bk >> 20) & 63u) - static_cast<int>(rr[3]));
+        }
+        return make_float2(av, bv);
+      };
+      // the same for a candidate of this chunk named by its flat index: its
+      // chunk row is the live position of its slot
+      const auto terms_of_flat = [&](uint32_t flat) __attribute__((always_inline)) {
+        const uint32_t slot = flat / static_cast<uint32_t>(W), c = flat - slot * static_cast<uint32_t>(W);
+        uint32_t i = 0u, row = 0u;
+#pragma unroll 1
+        for (int q = 0; q < kc; ++q) {
+          const uint32_t z = s_row[(cs + q) * kRowWords + 2];
+          if ((CACHE ? (z & 0xFFu) : z) == slot) {
+            i = static_cast<uint32_t>(q);
+            row = (z >> 8) & 0xFFu;
+          }
+        }
+        return cand_terms(i, c, row);
+      };
       // LM entry (staged, or the token's unigram state) and boosting key of
       // candidate (i, jj), re-read from the rows for the few that are kept
       // rather than held in registers from the scoring
@@ -1031,6 +1120,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         }
       }
       __syncthreads();  // C: pool complete
+      if constexpr (rep) {
+        // repeat-scoring variant: the terms of this chunk's survivors, while
+        // its rows are in place
+        const int n = min(s_nbuf, kCap);
+        for (int e = carry + tid; e < n; e += kThreads) s_pinc[e] = terms_of_flat(s_pool[e].y);
+        __syncthreads();
+      }
 
       // ---- R. exact rank of the pool: reserved region P + survivors ----
       // The best K go to region Q in rank order; after the last chunk the
@@ -1076,9 +1172,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
             if (last_chunk) {
               succ_end(sp, eq.x);
-              if (own && myrank < K) store_rec(nrec + myrank * RW, sp.r);
+              if (own && myrank < K) {
+                store_rec(nrec + myrank * RW, sp.r);
+                if (rep && sp.emit) put_terms(nrec + myrank * RW, (lane < K) ? s_rinc[P][lane] : s_pinc[lane - K]);
+              }
             } else if (own && myrank < K) {
               s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
+              if (rep) s_rinc[Q][myrank] = (lane < K) ? s_rinc[P][lane] : s_pinc[lane - K];
             }
           } else {
             // blocks of 64 entries: this wave ranks entries qb + (wave + 8u)
@@ -1122,6 +1222,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               // winners to region Q in rank order (after the last chunk their
               // successor records are built below, in one pass)
               if (win) s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
+              if (rep && win) s_rinc[Q][myrank] = (q < K) ? s_rinc[P][q] : s_pinc[q - K];
             }
             if (last_chunk) {
               __syncthreads();  // region Q complete
@@ -1134,6 +1235,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               succ_begin(act, e.y, e.z, e.w, prec, sp);
               succ_end(sp, e.x);
               if (act) store_rec(nrec + tid * RW, sp.r);
+              if (rep && act && sp.emit) put_terms(nrec + tid * RW, s_rinc[Q][tid]);
             }
           }
         } else {
@@ -1218,16 +1320,30 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   bk = (be >= genhi) ? be : p.bt_root_key[c];
                 }
                 s_res[Q][it] = make_uint4(__float_as_uint(wx), wflat, lmt, bk);
+                // terms taken after the extraction, from this chunk's rows
+                if (rep) s_rinc[Q][it] = make_float2(__builtin_nanf(""), 0.0f);
               } else if (who < 1000) {
                 s_res[Q][it] = s_res[P][who - 100];
+                if (rep) s_rinc[Q][it] = s_rinc[P][who - 100];
               } else {
                 s_res[Q][it] = s_pool[who - 1000];
+                if (rep) s_rinc[Q][it] = s_pinc[who - 1000];
               }
             }
             prev = gbest;
             ++nk;
           }
           nfin = nk;
+          if constexpr (rep) {
+            // the terms of the winners taken from this chunk's candidates
+            // (the later barriers order them before their readers)
+            __syncthreads();
+            if (tid < nk && __builtin_isnan(s_rinc[Q][tid].x)) {
+              const uint32_t flat = s_res[Q][tid].y;
+              // a token (blank winners carry no terms)
+              if (flat % static_cast<uint32_t>(W) < static_cast<uint32_t>(V)) s_rinc[Q][tid] = terms_of_flat(flat);
+            }
+          }
           if (last_chunk) {
             __syncthreads();  // region Q complete
             // rank tid (waves 0 .. SPL-1)
@@ -1238,6 +1354,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             succ_begin(act, e.y, e.z, e.w, prec, sp);
             succ_end(sp, e.x);
             if (act) store_rec(nrec + tid * RW, sp.r);
+            if (rep && act && sp.emit) put_terms(nrec + tid * RW, s_rinc[Q][tid]);
           }
         }
         // ranks [nfin, K) hold no candidate (the next chunk reads all K)
@@ -1985,56 +2102,66 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   }
 }
 
-template <int LPT, int NLEV, int SPL, bool SKIP>
+template <int LPT, int NLEV, int SPL, bool SKIP, bool REP>
 hipError_t launch_skip(const KernelParams& p, hipStream_t s) {
   dim3 grid(p.B), block(kThreads);
   constexpr bool kCacheable = SPL == 1 && !SKIP && LPT >= 2 && NLEV > 0;
-  if (p.bt_nodes != nullptr)
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP, false>), grid, block, 0, s, p);
-  else if (kCacheable && p.lm_states_below_2p23 && !(p.flags & kFlagNoRowCache))
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, kCacheable>), grid, block, 0, s, p);
-  else
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, false>), grid, block, 0, s, p);
+  if constexpr (REP) {
+    // the repeat-scoring variant reads uncached rows; with neither an LM nor
+    // boosting it has nothing to repeat (the caller takes the default kernel)
+    if (p.bt_nodes != nullptr) {
+      hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP, false, true>), grid, block, 0, s, p);
+    } else {
+      if constexpr (NLEV < 0) return hipErrorInvalidValue;
+      else hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, false, true>), grid, block, 0, s, p);
+    }
+  } else if (p.bt_nodes != nullptr) {
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP, false, false>), grid, block, 0, s, p);
+  } else if (kCacheable && p.lm_states_below_2p23 && !(p.flags & kFlagNoRowCache)) {
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, kCacheable, false>), grid, block, 0, s, p);
+  } else {
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, false, false>), grid, block, 0, s, p);
+  }
   return hipGetLastError();
 }
 
-template <int LPT, int NLEV, int SPL>
+template <int LPT, int NLEV, int SPL, bool REP>
 hipError_t launch_nlev(const KernelParams& p, hipStream_t s) {
   // beams of more than one chunk (16 / LPT rows) skip ranks
   if constexpr (SPL > 1) {
-    return launch_skip<LPT, NLEV, SPL, true>(p, s);
+    return launch_skip<LPT, NLEV, SPL, true, REP>(p, s);
   } else {
-    if (p.K > 16 / LPT) return launch_skip<LPT, NLEV, SPL, true>(p, s);
-    return launch_skip<LPT, NLEV, SPL, false>(p, s);
+    if (p.K > 16 / LPT) return launch_skip<LPT, NLEV, SPL, true, REP>(p, s);
+    return launch_skip<LPT, NLEV, SPL, false, REP>(p, s);
   }
 }
 
-template <int LPT, int SPL>
+template <int LPT, int SPL, bool REP>
 hipError_t launch_spl(const KernelParams& p, hipStream_t s) {
-  if (p.lm_states == nullptr && p.lm_arcs == nullptr) return launch_nlev<LPT, -1, SPL>(p, s);
+  if (p.lm_states == nullptr && p.lm_arcs == nullptr) return launch_nlev<LPT, -1, SPL, REP>(p, s);
   switch (p.lm_nlev) {
-    case 0: return launch_nlev<LPT, 0, SPL>(p, s);
-    case 1: return launch_nlev<LPT, 1, SPL>(p, s);
-    case 2: return launch_nlev<LPT, 2, SPL>(p, s);
-    case 3: return launch_nlev<LPT, 3, SPL>(p, s);
-    case 4: return launch_nlev<LPT, 4, SPL>(p, s);
-    case 5: return launch_nlev<LPT, 5, SPL>(p, s);
-    case 6: return launch_nlev<LPT, 6, SPL>(p, s);
-    case 7: return launch_nlev<LPT, 7, SPL>(p, s);
+    case 0: return launch_nlev<LPT, 0, SPL, REP>(p, s);
+    case 1: return launch_nlev<LPT, 1, SPL, REP>(p, s);
+    case 2: return launch_nlev<LPT, 2, SPL, REP>(p, s);
+    case 3: return launch_nlev<LPT, 3, SPL, REP>(p, s);
+    case 4: return launch_nlev<LPT, 4, SPL, REP>(p, s);
+    case 5: return launch_nlev<LPT, 5, SPL, REP>(p, s);
+    case 6: return launch_nlev<LPT, 6, SPL, REP>(p, s);
+    case 7: return launch_nlev<LPT, 7, SPL, REP>(p, s);
     default: return hipErrorInvalidValue;
   }
 }
 
 // beams above 64 take two slots per lane (vocabularies of at most 1024
 // tokens; the host rejects the rest)
-template <int LPT>
+template <int LPT, bool REP>
 hipError_t launch_lpt_impl(const KernelParams& p, hipStream_t s) {
   if constexpr (LPT <= 2) {
-    if (p.K > 64) return launch_spl<LPT, 2>(p, s);
+    if (p.K > 64) return launch_spl<LPT, 2, REP>(p, s);
   } else {
     if (p.K > 64) return hipErrorInvalidValue;
   }
-  return launch_spl<LPT, 1>(p, s);
+  return launch_spl<LPT, 1, REP>(p, s);
 }
 
 }  // namespace detail

@@ -243,6 +243,10 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
     wave_lds_fence();
   };
 
+  // repeat-scoring variant: the terms the last emitted token received
+  const bool rep = (HAS_LM || HAS_BT) && (p.flags & kFlagRepeatScore) != 0;
+  float ral = 0.0f, rwb = 0.0f;
+
   // Score one frame; returns true when the winner emits a token (the caller
   // then refills).  Sets `dead` when every candidate is -inf.
   auto step = [&](const float (&d)[NJ], float dbl) -> bool {
@@ -259,6 +263,28 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
       if (x > xb) {
         xb = x;
         jb = j;
+      }
+    }
+    if (rep && last != V && lane == lane_of(last)) {
+      // the lane holding the repeated token takes its best again, with the
+      // repeat scored x = ((s + D) + fl(alpha*LM)) + fl(w*BT)
+      xb = kNegInf;
+      jb = 0;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int c = label_of(lane, j);
+        const float x0 = s + d[j];
+        float x1 = x0 + beta;
+        if (HAS_LM) x1 = x1 + s_av[c];
+        if (HAS_BT) x1 = x1 + s_bv[c];
+        float xr = x0;
+        if (HAS_LM) xr = xr + ral;
+        if (HAS_BT) xr = xr + rwb;
+        const float x = (c != last) ? x1 : xr;
+        if (x > xb) {
+          xb = x;
+          jb = j;
+        }
       }
     }
     const float g = wave_max(xb);
@@ -291,6 +317,11 @@ __global__ void __launch_bounds__(64) greedy_kernel(KernelParams p) {
     if (emit) {
       if (lane == 0) ot[nout] = cw;
       ++nout;
+      if (rep) {
+        // read before the refill replaces the per-label terms
+        if (HAS_LM) ral = s_av[cw];
+        if (HAS_BT) rwb = s_bv[cw];
+      }
     }
     return emit;
   };

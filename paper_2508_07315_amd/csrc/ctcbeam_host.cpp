@@ -800,6 +800,7 @@ static_assert(CTCBEAM_MAX_K == ctcbeam::kMaxK, "beam size limit");
 static_assert(CTCBEAM_FLAG_LOGSUMEXP == ctcbeam::kFlagLogSumExp, "flag values");
 static_assert(CTCBEAM_FLAG_BOOST_ROLLBACK == ctcbeam::kFlagBoostRollback, "flag values");
 static_assert(CTCBEAM_FLAG_NO_ROW_CACHE == ctcbeam::kFlagNoRowCache, "flag values");
+static_assert(CTCBEAM_FLAG_REPEAT_SCORE == ctcbeam::kFlagRepeatScore, "flag values");
 
 namespace {
 
@@ -827,7 +828,8 @@ int decode_impl(const float* logprobs, const int32_t* lengths, int B, int T, int
   if (std::isnan(theta) || theta < 0.0f) return fail(1, "prune_theta must be >= 0 (or +inf)");
   if (std::isnan(alpha) || std::isnan(beta) || std::isnan(boost_w)) return fail(1, "NaN weight");
   const int flags = opts ? opts->flags : 0;
-  if (flags & ~(CTCBEAM_FLAG_LOGSUMEXP | CTCBEAM_FLAG_BOOST_ROLLBACK | CTCBEAM_FLAG_NO_ROW_CACHE))
+  if (flags & ~(CTCBEAM_FLAG_LOGSUMEXP | CTCBEAM_FLAG_BOOST_ROLLBACK | CTCBEAM_FLAG_NO_ROW_CACHE |
+                CTCBEAM_FLAG_REPEAT_SCORE))
     return fail(1, "unknown flag bits");
   if (B == 0) {
     // nothing to decode; a given workspace records the empty batch

@@ -21,6 +21,7 @@ constexpr uint32_t kExists = 0x80000000u;
 constexpr int kFlagLogSumExp = 1;      // recombination by log-sum-exp
 constexpr int kFlagBoostRollback = 2;  // pending boosting taken back at the end
 constexpr int kFlagNoRowCache = 4;     // LM key rows refilled for every beam every frame
+constexpr int kFlagRepeatScore = 8;    // repeated tokens get their LM / boosting terms again
 // Workspace: [header, kWsHeaderBytes][status word per utterance, padded to
 // 256 B][back-pointers [B, T, K] int32].  The header records the batch size
 // of the last decode that used the workspace, so that its status can be read
@@ -59,7 +60,7 @@ struct KernelParams {
   const int32_t* lengths;
   int B, T, V, K;
   float alpha, beta, boost_w, theta;
-  int flags;                 // kFlagLogSumExp | kFlagBoostRollback
+  int flags;                 // kFlag* bits
   // LM (null when disabled)
   const LmLevel* lm_states;
   const LmArc* lm_arcs;
@@ -101,6 +102,12 @@ hipError_t launch_lpt1(const KernelParams& p, hipStream_t stream);
 hipError_t launch_lpt2(const KernelParams& p, hipStream_t stream);
 hipError_t launch_lpt4(const KernelParams& p, hipStream_t stream);
 hipError_t launch_lpt8(const KernelParams& p, hipStream_t stream);
+// the same for the repeat-scoring variant (CTCBEAM_FLAG_REPEAT_SCORE with an
+// LM or boosting)
+hipError_t launch_lpt1_rep(const KernelParams& p, hipStream_t stream);
+hipError_t launch_lpt2_rep(const KernelParams& p, hipStream_t stream);
+hipError_t launch_lpt4_rep(const KernelParams& p, hipStream_t stream);
+hipError_t launch_lpt8_rep(const KernelParams& p, hipStream_t stream);
 
 // Greedy (one hypothesis) kernels by labels per lane: up to 256, 1024 and
 // 4096 tokens.
@@ -138,6 +145,13 @@ hipError_t launch_small(const KernelParams& p, hipStream_t stream);
 inline hipError_t launch_decode(const KernelParams& p, hipStream_t stream) {
   if (p.B == 0) return hipSuccess;
   if (small_beam_eligible(p)) return launch_small(p, stream);
+  // repeat scoring changes nothing without an LM or boosting
+  if ((p.flags & kFlagRepeatScore) && (p.lm_states != nullptr || p.lm_arcs != nullptr || p.bt_nodes != nullptr)) {
+    if (p.V <= 512) return launch_lpt1_rep(p, stream);
+    if (p.V <= 1024) return launch_lpt2_rep(p, stream);
+    if (p.V <= 2048) return launch_lpt4_rep(p, stream);
+    return launch_lpt8_rep(p, stream);
+  }
   if (p.V <= 512) return launch_lpt1(p, stream);
   if (p.V <= 1024) return launch_lpt2(p, stream);
   if (p.V <= 2048) return launch_lpt4(p, stream);

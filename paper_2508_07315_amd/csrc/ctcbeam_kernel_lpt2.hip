@@ -2,5 +2,5 @@
 #include "ctcbeam_decode.inl"
 
 namespace ctcbeam {
-hipError_t launch_lpt2(const KernelParams& p, hipStream_t s) { return detail::launch_lpt_impl<2>(p, s); }
+hipError_t launch_lpt2(const KernelParams& p, hipStream_t s) { return detail::launch_lpt_impl<2, false>(p, s); }
 }  // namespace ctcbeam

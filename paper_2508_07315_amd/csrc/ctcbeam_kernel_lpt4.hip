@@ -2,5 +2,5 @@
 #include "ctcbeam_decode.inl"
 
 namespace ctcbeam {
-hipError_t launch_lpt4(const KernelParams& p, hipStream_t s) { return detail::launch_lpt_impl<4>(p, s); }
+hipError_t launch_lpt4(const KernelParams& p, hipStream_t s) { return detail::launch_lpt_impl<4, false>(p, s); }
 }  // namespace ctcbeam

@@ -868,7 +868,7 @@ constexpr bool kDispatch = false;
 bool small_beam_eligible(const KernelParams& p) {
   if (!small::kDispatch) return false;
   if (p.bt_nodes != nullptr || p.K > small::kKmax || p.V > small::kVmax) return false;
-  if (p.flags & (kFlagNoRowCache | kFlagLogSumExp)) return false;
+  if (p.flags & (kFlagNoRowCache | kFlagLogSumExp | kFlagRepeatScore)) return false;
   const bool has_lm = p.lm_states != nullptr || p.lm_arcs != nullptr;
   // row entries name the reached state in 29 bits
   return !has_lm || (p.lm_nlev >= 1 && p.lm_nlev <= 7 && p.lm_n_states <= (int64_t(1) << small::kOrderShift));

@@ -1,5 +1,6 @@
 """GPU parity of the semantic variants (CTCBEAM_FLAG_LOGSUMEXP,
-CTCBEAM_FLAG_BOOST_ROLLBACK) against the CPU oracle with the same flags.
+CTCBEAM_FLAG_BOOST_ROLLBACK, and in the fuzzing CTCBEAM_FLAG_REPEAT_SCORE)
+against the CPU oracle with the same flags.
 
 Bar: tokens bit-exact, scores within 1e-4 (both sides run the same fp32
 log-sum-exp steps, so the difference is expected to be 0).
@@ -143,7 +144,8 @@ def test_variants_fuzz(seed):
     if rng.random() < 0.6:
         off, toks = _phrases(V, rng, int(rng.integers(1, 20)))
         bt, obt = P.ctcbeam_boost_build(V, off, toks), oracle.BT(V, off, toks)
-    flags = dict(logsumexp=bool(rng.random() < 0.8), boost_rollback=bool(rng.random() < 0.5))
+    flags = dict(logsumexp=bool(rng.random() < 0.8), boost_rollback=bool(rng.random() < 0.5),
+                 repeat_score=bool(rng.random() < 0.5))
     log(f"variants fuzz {seed}: B={B} T={T} V={V} K={K} theta={theta} {flags}")
     g = run(lp, lens, K, alpha, beta, bw, lm, bt, theta=theta, **flags)
     r = oracle.decode(lp, lens, K, alpha, beta, bw, theta=theta, lm=olm, bt=obt,
@@ -161,7 +163,7 @@ def test_unknown_flag_bits_are_rejected():
     sc = torch.empty((1,), dtype=torch.float32, device=device())
     o = P._Opts()
     o.prune_theta = math.inf
-    o.flags = 8
+    o.flags = 16
     rc = lib.ctcbeam_decode_ex(ctypes.c_void_p(d_lp.data_ptr()), ctypes.c_void_p(d_len.data_ptr()),
                                1, 3, 4, 2, 0.0, 0.0, 0.0, None, None, ctypes.c_void_p(ws.data_ptr()),
                                ws.numel(), ctypes.c_void_p(tok.data_ptr()), None,

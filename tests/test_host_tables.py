@@ -49,7 +49,8 @@ def test_flag_values_match_the_header():
     hdr = open(os.path.join(ROOT, "include", "ctcbeam.h")).read()
     flags = {m.group(1): int(m.group(2)) for m in re.finditer(r"#define CTCBEAM_FLAG_(\w+)\s+(\d+)", hdr)}
     assert flags == {"LOGSUMEXP": P.FLAG_LOGSUMEXP, "BOOST_ROLLBACK": P.FLAG_BOOST_ROLLBACK,
-                     "NO_ROW_CACHE": P.FLAG_NO_ROW_CACHE}, flags
+                     "NO_ROW_CACHE": P.FLAG_NO_ROW_CACHE,
+                     "REPEAT_SCORE": P.FLAG_REPEAT_SCORE}, flags
     assert len(set(flags.values())) == len(flags)
     assert all(v & (v - 1) == 0 for v in flags.values())  # one bit each
 
