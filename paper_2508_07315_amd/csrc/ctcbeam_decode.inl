@@ -162,6 +162,25 @@ __device__ __forceinline__ bool dup_by_sort(uint64_t key, int lane, uint32_t& lo
   return __builtin_amdgcn_ds_permute(static_cast<int>(sl) << 2, d ? 1 : 0) != 0;
 }
 
+// Per-phase clocks (profiling builds, -DCTCBEAM_PHASE_CLOCKS): each wave adds
+// the s_memtime cycles of every phase of every frame (fill, barrier A,
+// candidates, barrier B, filter, barrier C, rank, barrier D, update; then the
+// frame and chunk counts) and writes them after the [B, 8] statistics as
+// [B, kWaves, kPhaseWords] int64.  Product builds compile none of it.
+constexpr int kPhaseWords = 16;
+#ifdef CTCBEAM_PHASE_CLOCKS
+#define CTCBEAM_PHASE_MARK(k)                          \
+  do {                                                 \
+    const uint64_t now_ = __builtin_amdgcn_s_memtime(); \
+    ph_acc[k] += now_ - ph_t0;                         \
+    ph_t0 = now_;                                      \
+  } while (0)
+#else
+#define CTCBEAM_PHASE_MARK(k) \
+  do {                        \
+  } while (0)
+#endif
+
 // SPL = beam slots per lane: slot j lives in lane j % 64, register set
 // j / 64 (SPL = 2 serves beams of 65..128).  SKIP: ranks of chunks before
 // the last are skipped while the survivor pool has room (beams above one
@@ -322,7 +341,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     btpot[h] = 0;
     alive[h] = h == 0 && j == 0;
   }
+#ifdef CTCBEAM_PHASE_CLOCKS
+  // profiling builds: the stats buffer takes the phase clocks, and the
+  // counters stay off so that the phases time what a plain launch runs
+  const bool want_stats = false;
+#else
   const bool want_stats = p.stats != nullptr;
+#endif
   if (j == 0) {
     if (HAS_LM) {
 #pragma unroll
@@ -494,6 +519,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   uint32_t gen = 0u;
   int mpar = 0;  // reserved region holding the pool's reserved entries
   __syncthreads();
+#ifdef CTCBEAM_PHASE_CLOCKS
+  uint64_t ph_acc[kPhaseWords] = {};
+  uint64_t ph_t0 = __builtin_amdgcn_s_memtime();
+#endif
 
   for (int t = 0; t < L; ++t) {
     // ---- rotate and prefetch the log-prob row ----
@@ -750,7 +779,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           }
         }
       }
+      CTCBEAM_PHASE_MARK(0);
       __syncthreads();  // A: rows complete
+      CTCBEAM_PHASE_MARK(1);
 
       // ---- C. candidates ----
       // chunk row i is live position cs + i; its beam record is read with
@@ -1010,7 +1041,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       };
       float tblank = 0.0f;
       if constexpr (kSmallK) tblank = blank_bound();
+      CTCBEAM_PHASE_MARK(2);
       __syncthreads();  // B: bound inputs, blanks, pool reset
+      CTCBEAM_PHASE_MARK(3);
 
       // ---- T. bound and filter ----
       {
@@ -1119,7 +1152,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           }
         }
       }
+      CTCBEAM_PHASE_MARK(4);
       __syncthreads();  // C: pool complete
+      CTCBEAM_PHASE_MARK(5);
       if constexpr (rep) {
         // repeat-scoring variant: the terms of this chunk's survivors, while
         // its rows are in place
@@ -1139,6 +1174,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       if (SKIP && !last_chunk && !s_overflow && npool <= kCap / 2) {  // uniform
         carry = npool;
         cs += kc;
+#ifdef CTCBEAM_PHASE_CLOCKS
+        ph_acc[10] += 1;  // chunks
+#endif
         continue;
       }
       {
@@ -1361,7 +1399,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         if (!last_chunk && (SPL > 1 || wave == 0) && tid >= nfin && tid < K)
           s_res[Q][tid] = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
       }
+      CTCBEAM_PHASE_MARK(6);
       __syncthreads();  // D: best K of the chunk in region Q
+      CTCBEAM_PHASE_MARK(7);
+#ifdef CTCBEAM_PHASE_CLOCKS
+      ph_acc[10] += 1;  // chunks
+#endif
       mpar ^= 1;
       carry = 0;
       if (ch + 1 < nch && nfin >= K) tau_run = fmaxf(tau_run, __uint_as_float(s_res[mpar][K - 1].x));
@@ -1432,7 +1475,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       }
       if (dup) x = kNegInf;
       const bool nalive = alive0 && !dup;
-      if (wave == 0 && j < K) bpb[static_cast<size_t>(t) * K + j] = valid ? static_cast<int32_t>(rec[kRBp]) : -1;
+      // back-pointers and beam records from waves 1 and 2: wave 0 carries the
+      // frame's longest chain, and a store would hold its next load wait
+      // (vmcnt counts stores and loads in issue order)
+      if (wave == 1 && j < K) bpb[static_cast<size_t>(t) * K + j] = valid ? static_cast<int32_t>(rec[kRBp]) : -1;
       // new state
       sc[0] = x;
       last[0] = nlast;
@@ -1535,7 +1581,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           mm = __ballot(miss);
         }
       }
-      if (wave == 0 && nalive) put_row(lp, 0);
+      if (wave == 2 && nalive) put_row(lp, 0);
       // chunk plan: live slots in slot order, at most kcmax beams and
       // kLmStage staged arcs per chunk (cached rows stage nothing)
       if constexpr (CACHE) {
@@ -1680,7 +1726,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         if (dup[h]) x[h] = kNegInf;
         nalive[h] = alive0[h] && !dup[h];
         const int js = j + 64 * h;
-        if (wave == 0 && js < K)
+        if (wave == 1 && js < K)
           bpb[static_cast<size_t>(t) * K + js] = valid[h] ? static_cast<int32_t>(rec[h][kRBp]) : -1;
         // new state
         sc[h] = x[h];
@@ -1737,7 +1783,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         const uint64_t amask = __ballot(nalive[h]);
         lp[h] = na + __popcll(amask & lmlt);
         na += __popcll(amask);
-        if (wave == 0 && nalive[h]) put_row(lp[h], h);
+        if (wave == 2 && nalive[h]) put_row(lp[h], h);
         ia[h] = tota + wave_incl_scan(acnt[h], lane);
         tota = rdlane(ia[h], 63);
       }
@@ -1780,7 +1826,18 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       }
     }
     }
+    CTCBEAM_PHASE_MARK(8);
+#ifdef CTCBEAM_PHASE_CLOCKS
+    ph_acc[9] += 1;  // frames
+#endif
   }
+#ifdef CTCBEAM_PHASE_CLOCKS
+  if (p.stats && lane == 0) {
+    int64_t* pw = p.stats + static_cast<size_t>(p.B) * 8 + (static_cast<size_t>(b) * kWaves + wave) * kPhaseWords;
+#pragma unroll
+    for (int q = 0; q < kPhaseWords; ++q) pw[q] = static_cast<int64_t>(ph_acc[q]);
+  }
+#endif
 
   // single-slot and general forms kept apart, as for the beam update
   if constexpr (SPL == 1) {
