@@ -38,8 +38,8 @@ def _run(cmd):
 
 KERNEL_UNITS = ["ctcbeam_kernel_lpt1.hip", "ctcbeam_kernel_lpt2.hip", "ctcbeam_kernel_lpt4.hip",
                 "ctcbeam_kernel_lpt8.hip", "ctcbeam_kernel_lpt1_rep.hip", "ctcbeam_kernel_lpt2_rep.hip",
-                "ctcbeam_kernel_lpt4_rep.hip", "ctcbeam_kernel_lpt8_rep.hip", "ctcbeam_greedy_nj4.hip", "ctcbeam_greedy_nj16.hip",
-                "ctcbeam_greedy_nj64.hip", "ctcbeam_workspace.hip",
+                "ctcbeam_kernel_lpt4_rep.hip", "ctcbeam_kernel_lpt8_rep.hip", "ctcbeam_greedy_v256.hip", "ctcbeam_greedy_v1024.hip",
+                "ctcbeam_greedy_v4096.hip", "ctcbeam_workspace.hip",
                 "ctcbeam_noalloc.hip", "ctcbeam_small.hip"]
 
 

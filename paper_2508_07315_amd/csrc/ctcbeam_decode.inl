@@ -162,24 +162,11 @@ __device__ __forceinline__ bool dup_by_sort(uint64_t key, int lane, uint32_t& lo
   return __builtin_amdgcn_ds_permute(static_cast<int>(sl) << 2, d ? 1 : 0) != 0;
 }
 
-// Per-phase clocks (profiling builds, -DCTCBEAM_PHASE_CLOCKS): each wave adds
-// the s_memtime cycles of every phase of every frame (fill, barrier A,
-// candidates, barrier B, filter, barrier C, rank, barrier D, update; then the
-// frame and chunk counts) and writes them after the [B, 8] statistics as
-// [B, kWaves, kPhaseWords] int64.  Product builds compile none of it.
-constexpr int kPhaseWords = 16;
-#ifdef CTCBEAM_PHASE_CLOCKS
-#define CTCBEAM_PHASE_MARK(k)                          \
-  do {                                                 \
-    const uint64_t now_ = __builtin_amdgcn_s_memtime(); \
-    ph_acc[k] += now_ - ph_t0;                         \
-    ph_t0 = now_;                                      \
-  } while (0)
-#else
-#define CTCBEAM_PHASE_MARK(k) \
-  do {                        \
-  } while (0)
-#endif
+// Per-phase clocks (profiling builds, -DCTCBEAM_PHASE_CLOCKS; the macro is in
+// ctcbeam_internal.h): each wave adds the s_memtime cycles of every phase of
+// every frame (fill, barrier A, candidates, barrier B, filter, barrier C,
+// rank, barrier D, update; then the frame and chunk counts) and writes them
+// after the [B, 8] statistics as [B, kWaves, kPhaseWords] int64.
 
 // SPL = beam slots per lane: slot j lives in lane j % 64, register set
 // j / 64 (SPL = 2 serves beams of 65..128).  SKIP: ranks of chunks before

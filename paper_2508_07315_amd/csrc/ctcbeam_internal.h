@@ -31,6 +31,24 @@ constexpr uint32_t kWsMagic = 0x42435443u;  // "CTCB"
 
 // LM state record, one per chain level l (context of length l+1):
 //   {arc_begin, arc_count | kExists, backoff bits}
+// Per-phase clocks of the kernels in profiling builds (-DCTCBEAM_PHASE_CLOCKS):
+// a kernel declares uint64_t ph_acc[kPhaseWords] and ph_t0, and each
+// CTCBEAM_PHASE_MARK(k) adds the s_memtime cycles since the previous mark to
+// word k.  Product builds compile none of it.
+constexpr int kPhaseWords = 16;
+#ifdef CTCBEAM_PHASE_CLOCKS
+#define CTCBEAM_PHASE_MARK(k)                          \
+  do {                                                 \
+    const uint64_t now_ = __builtin_amdgcn_s_memtime(); \
+    ph_acc[k] += now_ - ph_t0;                         \
+    ph_t0 = now_;                                      \
+  } while (0)
+#else
+#define CTCBEAM_PHASE_MARK(k) \
+  do {                        \
+  } while (0)
+#endif
+
 struct LmLevel {
   uint32_t begin;
   uint32_t count;   // low 31 bits: arcs; bit 31: the context is an entry
@@ -109,20 +127,20 @@ hipError_t launch_lpt2_rep(const KernelParams& p, hipStream_t stream);
 hipError_t launch_lpt4_rep(const KernelParams& p, hipStream_t stream);
 hipError_t launch_lpt8_rep(const KernelParams& p, hipStream_t stream);
 
-// Greedy (one hypothesis) kernels by labels per lane: up to 256, 1024 and
-// 4096 tokens.
-hipError_t launch_greedy_nj4(const KernelParams& p, hipStream_t stream);
-hipError_t launch_greedy_nj16(const KernelParams& p, hipStream_t stream);
-hipError_t launch_greedy_nj64(const KernelParams& p, hipStream_t stream);
+// Greedy (one hypothesis) kernels by vocabulary: up to 256 tokens (one wave
+// per utterance), 1024 and 4096 tokens (four waves).
+hipError_t launch_greedy_v256(const KernelParams& p, hipStream_t stream);
+hipError_t launch_greedy_v1024(const KernelParams& p, hipStream_t stream);
+hipError_t launch_greedy_v4096(const KernelParams& p, hipStream_t stream);
 
 // Writes the header of an empty batch (B = 0: no decode kernel runs).
 hipError_t launch_ws_header(uint32_t* hdr, int B, hipStream_t stream);
 
 inline hipError_t launch_greedy(const KernelParams& p, hipStream_t stream) {
   if (p.B == 0) return hipSuccess;
-  if (p.V <= 256) return launch_greedy_nj4(p, stream);
-  if (p.V <= 1024) return launch_greedy_nj16(p, stream);
-  return launch_greedy_nj64(p, stream);
+  if (p.V <= 256) return launch_greedy_v256(p, stream);
+  if (p.V <= 1024) return launch_greedy_v1024(p, stream);
+  return launch_greedy_v4096(p, stream);
 }
 
 // The 1-best decode of ctcbeam_decode_ex into a given workspace (host side,

@@ -5,11 +5,14 @@ Build the profiling flavour first (``python -m paper_2508_07315_amd.build_lib
 counters at every phase boundary), then on a GPU:
 
     python -m paper_2508_07315_amd.phase_profile --config 3 [--beam K] [--theta 12]
+    python -m paper_2508_07315_amd.phase_profile --config 3 --mode greedy
 
-Prints, per phase of the frame step (fill, barrier A, candidates, barrier B,
-filter, barrier C, rank, barrier D, update), the mean cycles per frame of each
+Prints, per phase of the frame step (beam search: fill, barrier A,
+candidates, barrier B, filter, barrier C, rank, barrier D, update; greedy:
+scoring, the wave's best, the exchange barrier, the decision, chain headers +
+fold, continuations, log-prob row loads), the mean cycles per frame of each
 wave, averaged over the utterances (weighted by their frames), and the mean
-chunks per frame.  Inputs are the seeded workloads of ``workloads``.
+chunks (refills) per frame.  Inputs are the seeded workloads of ``workloads``.
 """
 from __future__ import annotations
 
@@ -18,7 +21,8 @@ import math
 import os
 import sys
 
-PHASES = ["fill", "bar A", "cand", "bar B", "filter", "bar C", "rank", "bar D", "update"]
+PHASES = {"beam": ["fill", "bar A", "cand", "bar B", "filter", "bar C", "rank", "bar D", "update"],
+          "greedy": ["score", "best", "barrier", "decide", "hdr+fold", "arcs", "rows"]}
 WAVES = 8
 WORDS = 16
 
@@ -29,6 +33,7 @@ def main(argv=None):
     ap.add_argument("--beam", type=int, default=0, help="beam size (default: the workload's)")
     ap.add_argument("--theta", type=float, default=math.inf)
     ap.add_argument("--batch", type=int, default=0)
+    ap.add_argument("--mode", choices=("beam", "greedy"), default="beam")
     args = ap.parse_args(argv)
 
     root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -61,18 +66,23 @@ def main(argv=None):
     theta = args.theta if not math.isinf(args.theta) else w.theta
     for _ in range(2):  # the second launch is measured (the first warms caches and code)
         buf.zero_()
-        P.ctcbeam_decode_ex(lp, lens, w.K, w.alpha, w.beta, w.boost_w, lm, bt, theta=theta,
-                            stats=stats)
+        if args.mode == "greedy":
+            P.ctcbeam_greedy_decode(lp, lens, w.alpha, w.beta, w.boost_w, lm, bt, stats=stats)
+        else:
+            P.ctcbeam_decode_ex(lp, lens, w.K, w.alpha, w.beta, w.boost_w, lm, bt, theta=theta,
+                                stats=stats)
         torch.cuda.synchronize()
     ph = buf[B * 8:].view(B, WAVES, WORDS).cpu().numpy().astype(np.float64)
     frames = ph[:, 0, 9]
     chunks = ph[:, 0, 10]
     nf = frames.sum()
-    print(f"{w.name} K={w.K} theta={theta}: {int(nf)} frames, {chunks.sum() / max(nf, 1):.2f} chunks/frame")
+    what = "refills" if args.mode == "greedy" else "chunks"
+    print(f"{w.name} {args.mode} K={1 if args.mode == 'greedy' else w.K} theta={theta}: {int(nf)} frames, "
+          f"{chunks.sum() / max(nf, 1):.2f} {what}/frame")
     print("cycles per frame by wave (mean over utterances, weighted by frames)")
     print("phase    " + " ".join(f"{'w%d' % q:>7s}" for q in range(WAVES)) + "     mean")
     tot = np.zeros(WAVES)
-    for k, name in enumerate(PHASES):
+    for k, name in enumerate(PHASES[args.mode]):
         per = ph[:, :, k].sum(axis=0) / max(nf, 1)
         tot += per
         print(f"{name:8s} " + " ".join(f"{v:7.0f}" for v in per) + f"  {per.mean():7.0f}")
