@@ -155,8 +155,7 @@ int decode_with_workspace(const float* logprobs, const int32_t* lengths, int B, 
 int set_last_error(int code, const char* msg);
 
 // Small-beam decoder (ctcbeam_small.inl): beams of at most 8, at most 1024
-// tokens, an n-gram LM of 1..7 backoff levels or none, no boosting, max
-// recombination, LM rows kept across frames.
+// tokens, no LM and no boosting, max recombination.
 bool small_beam_eligible(const KernelParams& p);
 hipError_t launch_small(const KernelParams& p, hipStream_t stream);
 

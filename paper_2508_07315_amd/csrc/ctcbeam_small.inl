@@ -1,24 +1,17 @@
-// Small-beam decoder: K <= 8 hypotheses, V <= 1024 tokens, an n-gram LM or
-// none, no phrase boosting (gfx950).  Included by ctcbeam_small.hip.
+// Small-beam decoder: K <= 8 hypotheses, V <= 1024 tokens, no LM and no
+// phrase boosting (gfx950).  Included by ctcbeam_small.hip.
 //
 // Same search as the general decoder (FlexCTC Algorithm 1 with the Eq. 1
-// fold x = s_k + D[c]; x += beta; x += fl(alpha*LM) for emitting labels;
-// TopK by (score desc, flat index asc); pruning; LM state update;
-// recombination; LM.Final; read-out of the hypothesis trie, Sec. III-A), laid
-// out for the beam sizes of the paper's main tables (K = 4..8):
+// fold x = s_k + D[c], x += beta for emitting labels; TopK by (score desc,
+// flat index asc); pruning; recombination; read-out of the hypothesis trie,
+// Sec. III-A), laid out for the beam sizes of the paper's main tables
+// (K = 4..8) without a language model:
 //
 // * one workgroup of 4 wave64 per utterance, one wave per SIMD; lane l of
 //   wave w scores labels c = 64w + l + 256j, j < 4, for every live beam;
-// * the beam itself (scores, transcript hashes, LM states and chain headers)
+// * the beam itself (scores, last labels, transcript hashes and lengths)
 //   lives in registers of wave 0 only (slot k in lane k): the selection and
-//   the update run once, in that wave, instead of in every wave;
-// * LM rows: 16 rows of 1024 64-bit entries (alpha * ln P(c | state) : the
-//   state reached by emitting c) in LDS, one LM state each, kept across
-//   frames and replaced least recently used.  A state new to the rows is
-//   filled by one wave: every token's unigram + backoff fold, then the
-//   explicit continuations of each backoff level in increasing order, as
-//   plain stores in program order, so the highest order wins without atomics
-//   or generation tags.
+//   the update run once, in that wave, instead of in every wave.
 //
 // Per frame: S (all waves) score every candidate in registers and publish
 // the maxima of (beam, wave) groups; barrier; F (all waves) take the K-th
@@ -26,10 +19,9 @@
 // a lower bound of the K-th best candidate and write the candidates at or
 // above it to per-wave survivor segments; barrier; R (wave 0) ranks the blank
 // candidates and the survivors exactly, builds the successors, prunes,
-// recombines, writes the back-pointers and assigns LM rows; barrier; L fills
-// rows of new LM states (one wave per row); barrier when a row was filled.
-// More than 64 ranked entries (mass ties) fall back to an exact K-step
-// extraction over all candidates.
+// recombines and writes the back-pointers; barrier.  More than 64 ranked
+// entries (mass ties) fall back to an exact K-step extraction over all
+// candidates.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -50,15 +42,8 @@ constexpr int kSW = kST / 64;        // waves
 constexpr int kLPL = 4;              // labels per lane
 constexpr int kVmax = kST * kLPL;    // 1024 labels (blank handled apart)
 constexpr int kKmax = 8;             // beam slots
-constexpr int kRows = 12;            // LM rows (LM states) kept in LDS
 constexpr int kSeg = 64;             // survivor entries per wave
-constexpr int kTileBatch = 4;        // arc tiles of 64 in flight per wave
-constexpr uint32_t kRowMask = (1u << kRows) - 1u;
-// LM row entry: high word = backoff order (0 fold, l + 1 for an arc of chain
-// level l) << 29 | state reached by emitting the token; low word = alpha *
-// ln P as float bits.  The 64-bit maximum of two entries keeps the higher order.
-constexpr int kOrderShift = 29;
-constexpr uint32_t kTgtMask = (1u << kOrderShift) - 1u;
+constexpr int kStage = 2048;         // 64-bit words of the traceback tiles
 
 // value of lane (lane ^ j) for compile-time j, with the lane masks
 // materialised where they are used (a frame loop would otherwise keep every
@@ -83,41 +68,26 @@ __device__ __forceinline__ uint32_t xlane(uint32_t v) {
 template <int J>
 __device__ __forceinline__ float xlanef(float v) { return __uint_as_float(xlane<J>(__float_as_uint(v))); }
 
-__device__ __forceinline__ uint64_t pack_entry(float av, uint32_t hi) {
-  return (static_cast<uint64_t>(hi) << 32) | __float_as_uint(av);
-}
-
-template <int NL>  // LM backoff-chain levels; 0: no LM
 __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
-  constexpr bool HAS_LM = NL > 0;
-  constexpr int NLA = HAS_LM ? NL : 1;
-  // LM rows [row][token] (no LM: only the traceback tiles)
-  constexpr int kBigU64 = HAS_LM ? kRows * kVmax : 2048;
-  __shared__ __align__(16) uint64_t s_big[kBigU64];
-  // LM state of each row; [frame & 1] is read by frame t, [frame & 1 ^ 1]
-  // written for frame t + 1
-  __shared__ __align__(16) uint32_t s_rtag[2][kRows];
+  // back-pointer tiles of the traceback
+  __shared__ __align__(16) uint64_t s_big[kStage];
 
   // this frame's candidates: [live position][thread] -> labels tid + 256 j
   __shared__ __align__(16) float4 s_cand[kKmax * kST];
-  __shared__ uint4 s_seg[kSW][kSeg];     // survivors: score bits, flat index, LM target
+  __shared__ uint4 s_seg[kSW][kSeg];     // survivors: score bits, flat index, 0, emits
   __shared__ int s_nseg[kSW];
   __shared__ int s_ovf;
   __shared__ float s_gmax[kSW * kKmax];  // (beam, wave) maxima
   // the beam as the scoring sees it, by live position (slot order; dead
-  // positions score -inf): score bits, last label, LM row * 1024, slot * W
+  // positions score -inf): score bits, last label, 0, slot * W
   __shared__ uint4 s_beam[2][kKmax];  // [frame & 1] read by frame t
   __shared__ int s_nlive;
-  // rows to fill: row, chain of its LM state
-  __shared__ int s_nfill;
-  __shared__ int s_frow[kKmax];
-  __shared__ LmLevel s_fch[kKmax][NLA];
   // exact extraction (fallback): winners in rank order; wave maxima
   __shared__ uint4 s_win[kKmax];
   __shared__ __align__(16) uint64_t s_key[64];  // ranked keys (wave 0)
   // the beam's slot records (wave 0 writes them after each update): hash lo,
-  // hi, length, LM state, then per chain level begin, count, backoff
-  constexpr int kSlotWords = (4 + 3 * NLA + 3) & ~3;
+  // hi, length
+  constexpr int kSlotWords = 4;
   __shared__ __align__(16) uint32_t s_slot[kKmax][kSlotWords];
   __shared__ uint64_t s_red[2][kSW];
   __shared__ int s_best, s_bestlen;
@@ -129,8 +99,7 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int b = blockIdx.x;
   const int V = p.V, W = V + 1, K = p.K, T = p.T;
-  const float alpha = p.alpha, beta = p.beta;
-  const uint32_t bos = p.lm_bos_state;
+  const float beta = p.beta;
   const bool want_stats = p.stats != nullptr;
 
   int L = p.lengths[b];
@@ -140,149 +109,34 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
   const float* Db = p.logprobs + static_cast<size_t>(b) * T * W;
   int32_t* bpb = p.bp + static_cast<size_t>(b) * T * K;
 
-  for (int i = tid; i < kBigU64; i += kST) s_big[i] = 0ull;  // tokens >= V stay finite
-  float rD[kLPL], rDn[kLPL], rUni[kLPL];
+  float rD[kLPL], rDn[kLPL];
 #pragma unroll
   for (int j = 0; j < kLPL; ++j) {
     const int c = tid + j * kST;
     rDn[j] = (c < V && L > 0) ? Db[c] : kNegInf;
     rD[j] = kNegInf;
-    rUni[j] = (HAS_LM && c < V) ? p.lm_unigram[c] : 0.0f;
   }
 
   // ---- the beam (wave 0, slot k in lane k) ----
   float sc = (lane == 0) ? 0.0f : kNegInf;
   int last = V, len = 0;
-  uint32_t hlo = 0u, hhi = 0u, lms = bos;
-  uint32_t lvb[NLA], lvc[NLA];
-  float lvbo[NLA];
-#pragma unroll
-  for (int l = 0; l < NLA; ++l) {
-    lvb[l] = 0u;
-    lvc[l] = 0u;
-    lvbo[l] = 0.0f;
-  }
-  if (HAS_LM && wave == 0 && lane == 0) {
-#pragma unroll
-    for (int l = 0; l < NL; ++l) {
-      const LmLevel hd = p.lm_states[static_cast<size_t>(bos) * NL + l];
-      lvb[l] = hd.begin;
-      lvc[l] = hd.count;
-      lvbo[l] = hd.bo;
-    }
-  }
+  uint32_t hlo = 0u, hhi = 0u;
 
   // counters (wave 0 lanes, summed at the end)
-  uint32_t st_alive = 0u, st_ls = 0u, st_la = 0u, st_emit = 0u;
-  if (tid < kRows) s_rtag[0][tid] = (tid == 0 && L > 0) ? bos : 0xFFFFFFFFu;
+  uint32_t st_alive = 0u, st_emit = 0u;
 
   if (tid < kKmax) {
-    // slot records: slot 0 is the initial beam (<s>), the others never parents
+    // slot records: slot 0 is the initial (empty) beam, the others never parents
 #pragma unroll
     for (int w = 0; w < kSlotWords; ++w) s_slot[tid][w] = 0u;
-    if (tid == 0) {
-      s_slot[0][3] = bos;
-#pragma unroll
-      for (int l = 0; l < NL; ++l) {
-        s_slot[0][4 + 3 * l] = lvb[l];
-        s_slot[0][5 + 3 * l] = lvc[l];
-        s_slot[0][6 + 3 * l] = __float_as_uint(lvbo[l]);
-      }
-    }
-  }
-  if (tid < kKmax)
     s_beam[0][tid] = make_uint4(__float_as_uint(tid == 0 ? 0.0f : kNegInf), static_cast<uint32_t>(V), 0u, 0u);
+  }
   if (tid == 0) {
     s_nlive = L > 0 ? 1 : 0;
-    s_nfill = (HAS_LM && L > 0) ? 1 : 0;
-    s_frow[0] = 0;
-#pragma unroll
-    for (int l = 0; l < NL; ++l) s_fch[0][l] = LmLevel{lvb[l], lvc[l], lvbo[l]};
     s_ovf = 0;
   }
   __syncthreads();
 
-  // ---- L: fill the rows of LM states new to the rows ----
-  // (1) every wave writes the unigram + backoff fold of its own tokens into
-  // each new row (order 0; the token's unigram state); barrier; (2) the
-  // explicit continuations of every (row, level) segment, in tiles of 64 that
-  // never straddle a segment, dealt round-robin to the waves and combined by a
-  // 64-bit maximum, so the highest order wins in any order.  The caller ends
-  // with a barrier.
-  auto fill_rows = [&]() __attribute__((always_inline)) {
-    if constexpr (HAS_LM) {
-      const int nf = __builtin_amdgcn_readfirstlane(s_nfill);
-      for (int f = 0; f < nf; ++f) {  // uniform
-        const uint32_t rb = static_cast<uint32_t>(s_frow[f]) * kVmax;
-        float bo[NL];
-#pragma unroll
-        for (int l = 0; l < NL; ++l) bo[l] = s_fch[f][l].bo;
-#pragma unroll
-        for (int j = 0; j < kLPL; ++j) {
-          const int c = tid + j * kST;
-          if (c < V) {
-            float v = rUni[j];
-#pragma unroll
-            for (int l = 0; l < NL; ++l) v = v + bo[l];
-            s_big[rb + c] = pack_entry(alpha * v, static_cast<uint32_t>(c));
-          }
-        }
-      }
-      __syncthreads();
-      // segment table: lane s < nf * NL holds (fill s / NL, level s % NL)
-      uint32_t sg_beg = 0u, sg_cnt = 0u, sg_rb = 0u;
-      if (lane < nf * NL) {
-        const int f = lane / NL, l = lane - f * NL;
-        const LmLevel h = s_fch[f][l];
-        sg_beg = h.begin;
-        sg_cnt = h.count & ~kExists;
-        sg_rb = static_cast<uint32_t>(s_frow[f]) * kVmax;
-      }
-      const int stl = static_cast<int>((sg_cnt + 63u) >> 6);
-      const int tincl = detail::wave_incl_scan(stl, lane);
-      const int texcl = tincl - stl;
-      const int ntile = rdlane(tincl, 63);
-      for (int g0 = wave; g0 < ntile; g0 += kSW * kTileBatch) {  // uniform per wave
-        LmArc a[kTileBatch];
-        uint32_t arb[kTileBatch];
-        int asg[kTileBatch];
-#pragma unroll
-        for (int u = 0; u < kTileBatch; ++u) {
-          const int g = g0 + u * kSW;
-          a[u].token = 0xFFFFFFFFu;
-          arb[u] = 0u;
-          asg[u] = 0;
-          if (g < ntile) {  // uniform
-            const int sg = static_cast<int>(__popcll(__ballot(tincl <= g)));
-            const uint32_t off = static_cast<uint32_t>(g - rdlane(texcl, sg)) * 64u + static_cast<uint32_t>(lane);
-            arb[u] = rdlane(sg_rb, sg);
-            asg[u] = sg;
-            if (off < rdlane(sg_cnt, sg)) a[u] = p.lm_arcs[rdlane(sg_beg, sg) + off];
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < kTileBatch; ++u) {
-          if (a[u].token < static_cast<uint32_t>(V)) {
-            const int f = asg[u] / NL, l = asg[u] - f * NL;
-            float v = a[u].logp;
-            // backoff weights of the levels above the arc's, innermost first
-#pragma unroll
-            for (int q = 1; q < NL; ++q)
-              if (q > l) v = v + s_fch[f][q].bo;
-            atomicMax(reinterpret_cast<unsigned long long*>(&s_big[arb[u] + a[u].token]),
-                      pack_entry(alpha * v, (static_cast<uint32_t>(l + 1) << kOrderShift) | a[u].target));
-          }
-        }
-      }
-    }
-  };
-  if (HAS_LM && L > 0) {
-    fill_rows();
-    __syncthreads();
-  }
-
-  // wave 0: round-robin start of the search for free LM rows
-  int rrow = 0;
   for (int t = 0; t < L; ++t) {
     const int cb = t & 1;  // double buffers read by this frame
     // labels past V read the row's blank and score -inf (the prefetched
@@ -303,13 +157,6 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
     for (int i = 0; i < kKmax; ++i) brec[i] = s_beam[cb][i];  // broadcast reads
     float cand[kKmax][kLPL];
     float rmax[kKmax];
-    // every row value in flight before the arithmetic
-    float lmv[kKmax][kLPL];
-#pragma unroll
-    for (int i = 0; i < kKmax; ++i)
-#pragma unroll
-      for (int j = 0; j < kLPL; ++j)
-        lmv[i][j] = HAS_LM ? __uint_as_float(reinterpret_cast<const uint32_t*>(s_big)[2u * (brec[i].z + tid + j * kST)]) : 0.0f;
 #pragma unroll
     for (int i = 0; i < kKmax; ++i) {
       const float si = __uint_as_float(brec[i].x);
@@ -318,8 +165,7 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
       for (int j = 0; j < kLPL; ++j) {
         const int c = tid + j * kST;
         const float x0 = si + rD[j];
-        float x = x0 + beta;
-        if constexpr (HAS_LM) x = x + lmv[i][j];
+        const float x = x0 + beta;
         // the repeat of the beam's last frame label emits nothing
         cand[i][j] = (c == lasti) ? x0 : x;
       }
@@ -387,9 +233,7 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
           const uint32_t c = static_cast<uint32_t>(tid + (r & 3) * kST);
           const float x = reinterpret_cast<const float*>(s_cand)[(i * kST + tid) * 4 + (r & 3)];
           const uint4 br = s_beam[cb][i];
-          uint32_t tgt = 0u;
-          if constexpr (HAS_LM) tgt = static_cast<uint32_t>(s_big[br.z + c] >> 32) & kTgtMask;
-          s_seg[wave][at++] = make_uint4(__float_as_uint(x), br.w + c, tgt, c != br.y ? 1u : 0u);
+          s_seg[wave][at++] = make_uint4(__float_as_uint(x), br.w + c, 0u, c != br.y ? 1u : 0u);
         }
       }
       if (lane == 0) s_nseg[wave] = tot;
@@ -453,9 +297,7 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
           } else {
             const uint32_t c = wcode & 1023u;
             const float x = reinterpret_cast<const float*>(s_cand)[(i * kST + (c & 255u)) * 4u + (c >> 8)];
-            uint32_t tgt = 0u;
-            if constexpr (HAS_LM) tgt = static_cast<uint32_t>(s_big[br.z + c] >> 32) & kTgtMask;
-            win = make_uint4(__float_as_uint(x), br.w + c, tgt, 0u);
+            win = make_uint4(__float_as_uint(x), br.w + c, 0u, 0u);
           }
           s_win[it] = win;
         }
@@ -469,7 +311,7 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
       // ---- entries (normal path): lane l < nlive the blank candidate of live
       // position l, then the four survivor segments ----
       float ex = kNegInf;
-      uint32_t eidx = 0xFFFFFFFFu, etgt = 0u;
+      uint32_t eidx = 0xFFFFFFFFu;
       if (!fallback) {
         if (lane < nlive) {
           const uint4 br = s_beam[cb][lane];
@@ -481,13 +323,11 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
           const uint4 v = s_seg[w][e];
           ex = __uint_as_float(v.x);
           eidx = v.y;
-          etgt = v.z;
         }
       } else if (lane < nfin) {
         const uint4 v = s_win[lane];
         ex = __uint_as_float(v.x);
         eidx = v.y;
-        etgt = v.z;
       }
       const bool evalid = ex != kNegInf;
       // parent slot, label, emission
@@ -519,27 +359,13 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
       const bool valid = lane < nfin;
       float x = __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(ex)));
       const int pk = __builtin_amdgcn_ds_bpermute(src << 2, static_cast<int>(epar & 7u) | (ec << 3) | ((eemit ? 1 : 0) << 14));
-      const uint32_t ntgt = static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src << 2, static_cast<int>(etgt)));
       const int par = pk & 7;
       const int c = (pk >> 3) & 2047;
       const bool emit = valid && ((pk >> 14) & 1);
       if (!valid) x = kNegInf;
-      // chain headers of an emitted token's LM state: in flight during the update
-      LmLevel eh[NLA];
-#pragma unroll
-      for (int l = 0; l < NL; ++l) eh[l] = p.lm_states[static_cast<size_t>(emit ? ntgt : bos) * NL + l];
 
-      // counters: the beams entering this frame and their LM chains
-      if (want_stats && lane < K && sc != kNegInf) {
-        st_alive += 1u;
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-          if (lvc[l] & kExists) {
-            st_ls += 1u;
-            st_la += lvc[l] & ~kExists;
-          }
-        }
-      }
+      // counters: the beams entering this frame
+      if (want_stats && lane < K && sc != kNegInf) st_alive += 1u;
 
       // successor of the parent slot (its record, from LDS)
       uint32_t prec[kSlotWords];
@@ -553,21 +379,11 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
       }
       const uint32_t plo = prec[0], phi = prec[1];
       const int plen = static_cast<int>(prec[2]);
-      const uint32_t plms = prec[3];
-      uint32_t pvb[NLA], pvc[NLA];
-      float pvbo[NLA];
-#pragma unroll
-      for (int l = 0; l < NL; ++l) {
-        pvb[l] = prec[4 + 3 * l];
-        pvc[l] = prec[5 + 3 * l];
-        pvbo[l] = __uint_as_float(prec[6 + 3 * l]);
-      }
       uint64_t h = (static_cast<uint64_t>(phi) << 32) | plo;
       const uint64_t hm = mix_token(h, static_cast<uint32_t>(c));
       h = emit ? hm : h;
       const int nlen = plen + (emit ? 1 : 0);
       const int nlast = valid ? c : V;
-      const uint32_t nlms = emit ? ntgt : plms;
 
       // prune (Algorithm 1: below best - theta -> -inf)
       const float lim = rdlane(x, 0) - p.theta;
@@ -589,159 +405,27 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
       len = nlen;
       hlo = static_cast<uint32_t>(h);
       hhi = static_cast<uint32_t>(h >> 32);
-      lms = nlms;
-      // chain headers: the loaded ones for an emission, else the parent's
-#pragma unroll
-      for (int l = 0; l < NL; ++l) {
-        lvb[l] = emit ? eh[l].begin : pvb[l];
-        lvc[l] = emit ? eh[l].count : pvc[l];
-        lvbo[l] = emit ? eh[l].bo : pvbo[l];
-      }
-      if (lane < K) {
-        uint32_t rec[kSlotWords];
-#pragma unroll
-        for (int w = 0; w < kSlotWords; ++w) rec[w] = 0u;
-        rec[0] = hlo;
-        rec[1] = hhi;
-        rec[2] = static_cast<uint32_t>(len);
-        rec[3] = lms;
-#pragma unroll
-        for (int l = 0; l < NL; ++l) {
-          rec[4 + 3 * l] = lvb[l];
-          rec[5 + 3 * l] = lvc[l];
-          rec[6 + 3 * l] = __float_as_uint(lvbo[l]);
-        }
-#pragma unroll
-        for (int w4 = 0; w4 < kSlotWords; w4 += 4)
-          *reinterpret_cast<uint4*>(&s_slot[lane][w4]) = make_uint4(rec[w4], rec[w4 + 1], rec[w4 + 2], rec[w4 + 3]);
-      }
+      if (lane < K) *reinterpret_cast<uint4*>(&s_slot[lane][0]) = make_uint4(hlo, hhi, static_cast<uint32_t>(len), 0u);
       const uint64_t am = __ballot(alive && lane < K);
-      int myrow = 0;
-      if constexpr (HAS_LM) {
-        // rows: a live slot whose state has a row keeps it; the first slot of
-        // each other state takes, in slot order, the least recently used rows
-        // no live slot holds, and later slots of that state share its row;
-        // those rows are filled below
-        const bool want = alive && lane < K;
-        int hit = -1;
-#pragma unroll
-        for (int r = kRows - 1; r >= 0; --r) hit = (s_rtag[cb][r] == nlms) ? r : hit;
-        hit = want ? hit : -1;
-        uint32_t ub = hit >= 0 ? (1u << hit) : 0u;
-        ub |= xlane<1>(ub);
-        ub |= xlane<2>(ub);
-        ub |= xlane<4>(ub);
-        const uint32_t used = rdlane(ub, 0);  // slots are lanes 0..7
-        const bool miss = want && hit < 0;
-        // a lower missing slot with the same state (row shifts; LM states are
-        // below 2^29, so all ones marks "none")
-        const uint32_t mkey = miss ? nlms : 0xFFFFFFFFu;
-        int dsh = 0;
-#define CTCBEAM_SHIFT_MATCH(D)                                                                         \
-  {                                                                                                    \
-    const uint32_t o = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(-1, static_cast<int>(mkey),   \
-                                                                         0x110 + (D), 0xF, 0xF, false)); \
-    dsh = (miss && o == mkey) ? (D) : dsh;                                                             \
-  }
-        CTCBEAM_SHIFT_MATCH(1) CTCBEAM_SHIFT_MATCH(2) CTCBEAM_SHIFT_MATCH(3) CTCBEAM_SHIFT_MATCH(4)
-        CTCBEAM_SHIFT_MATCH(5) CTCBEAM_SHIFT_MATCH(6) CTCBEAM_SHIFT_MATCH(7)
-#undef CTCBEAM_SHIFT_MATCH
-        const bool first = miss && dsh == 0;
-        const uint64_t fm = __ballot(first);
-        const int nf = static_cast<int>(__popcll(fm));
-        const int mrank = static_cast<int>(__popcll(fm & lanemask_lt()));
-        // free rows in round-robin order from the row after the last one
-        // taken: lane q (< kRows) is the q-th row from rrow
-        const uint32_t freem = ~used & kRowMask;
-        const uint32_t frot = ((freem >> rrow) | (freem << (kRows - rrow))) & kRowMask;
-        const int qrow = (lane + rrow) % kRows;
-        const bool fr = lane < kRows && ((frot >> (lane & 31)) & 1u);
-        const int lr = static_cast<int>(__popc(frot & ((1u << (lane & 31)) - 1u)));
-        // lane m of the table holds the free row of rank m
-        const int tbl = __builtin_amdgcn_ds_permute((fr ? lr : 63) << 2, qrow);
-        const int nrow = __builtin_amdgcn_ds_bpermute(mrank << 2, tbl);
-        int mr = hit >= 0 ? hit : (first ? nrow : 0);
-        // later slots of a new state: the row of the lowest slot with it
-#define CTCBEAM_SHIFT_ROW(D)                                                                             \
-  {                                                                                                      \
-    const int o = __builtin_amdgcn_update_dpp(0, mr, 0x110 + (D), 0xF, 0xF, false);                       \
-    mr = (dsh == (D)) ? o : mr;                                                                          \
-  }
-        CTCBEAM_SHIFT_ROW(1) CTCBEAM_SHIFT_ROW(2) CTCBEAM_SHIFT_ROW(3) CTCBEAM_SHIFT_ROW(4)
-        CTCBEAM_SHIFT_ROW(5) CTCBEAM_SHIFT_ROW(6) CTCBEAM_SHIFT_ROW(7)
-#undef CTCBEAM_SHIFT_ROW
-        if (first) {
-          s_frow[mrank] = nrow;
-#pragma unroll
-          for (int l = 0; l < NL; ++l) s_fch[mrank][l] = LmLevel{lvb[l], lvc[l], lvbo[l]};
-        }
-        // tags and ages for the next frame: row r in lane r
-        const int nxt = cb ^ 1;
-        const uint32_t ntg = lane < kRows ? s_rtag[cb][lane & 15] : 0xFFFFFFFFu;
-        const uint32_t mtg = static_cast<uint32_t>(__builtin_amdgcn_ds_permute((first ? nrow : 63) << 2, static_cast<int>(nlms)));
-        uint32_t nb = first ? (1u << nrow) : 0u;
-        nb |= xlane<1>(nb);
-        nb |= xlane<2>(nb);
-        nb |= xlane<4>(nb);
-        const uint32_t newm = rdlane(nb, 0);
-        if (lane < kRows) s_rtag[nxt][lane] = ((newm >> lane) & 1u) ? mtg : ntg;
-        if (nf > 0) rrow = (rdlane(tbl, nf - 1) + 1) % kRows;  // after the last row taken
-        if (lane == 0) s_nfill = nf;
-        myrow = mr;
-      }
       // the beam as the next frame's scoring sees it (positions past the
       // live slots score -inf)
       const int na = static_cast<int>(__popcll(am));
       if (alive && lane < K) {
         const int lp = static_cast<int>(__popcll(am & lanemask_lt()));
-        s_beam[cb ^ 1][lp] = make_uint4(__float_as_uint(sc), static_cast<uint32_t>(last),
-                                static_cast<uint32_t>(myrow * kVmax), static_cast<uint32_t>(lane * W));
+        s_beam[cb ^ 1][lp] = make_uint4(__float_as_uint(sc), static_cast<uint32_t>(last), 0u,
+                                        static_cast<uint32_t>(lane * W));
       }
       if (lane >= na && lane < kKmax)
         s_beam[cb ^ 1][lane] = make_uint4(__float_as_uint(kNegInf), static_cast<uint32_t>(V), 0u, 0u);
       if (lane == 0) s_nlive = na;
     }
-    __syncthreads();  // B3: beam table and rows to fill
-    if constexpr (HAS_LM) {
-      if (s_nfill > 0) {  // uniform
-        fill_rows();
-        __syncthreads();  // B4: rows complete
-      }
-    }
+    __syncthreads();  // B3: beam table
   }
 
-  // ---- LM.Final and the order of the final hypotheses (wave 0) ----
+  // ---- the order of the final hypotheses (wave 0) ----
   const bool nbest = p.nbest_scores != nullptr;
   if (wave == 0) {
-    float s = sc;
-    if (HAS_LM && lane < K && s != kNegInf) {
-      // ln P(</s> | state) through the backoff chain; </s> is the last arc
-      // of a state's sorted arcs when present
-      float v = p.lm_unigram[V];
-      int found = -1;
-      float fv = 0.0f;
-#pragma unroll
-      for (int l = NL - 1; l >= 0; --l) {
-        const uint32_t n = lvc[l] & ~kExists;
-        if (found < 0 && n > 0) {
-          const LmArc a = p.lm_arcs[lvb[l] + n - 1];
-          if (a.token == static_cast<uint32_t>(V)) {
-            found = l;
-            fv = a.logp;
-          }
-        }
-      }
-      if (found >= 0) {
-        v = fv;
-#pragma unroll
-        for (int l = 0; l < NL; ++l)
-          if (l > found) v = v + lvbo[l];
-      } else {
-#pragma unroll
-        for (int l = 0; l < NL; ++l) v = v + lvbo[l];
-      }
-      s = s + alpha * v;
-    }
+    const float s = sc;
     const float sj = lane < K ? s : kNegInf;
     // rank: final score descending, lowest slot on ties
     int rank = 0;
@@ -765,20 +449,18 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
       s_bestlen = blen;
     }
     if (want_stats) {
-      uint32_t a0 = st_alive, a1 = st_ls, a2 = st_la, a3 = st_emit;
+      uint32_t a0 = st_alive, a3 = st_emit;
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
         a0 += __shfl_xor(a0, off);
-        a1 += __shfl_xor(a1, off);
-        a2 += __shfl_xor(a2, off);
         a3 += __shfl_xor(a3, off);
       }
       if (lane == 0) {
         int64_t* so = p.stats + static_cast<size_t>(b) * 8;
         so[0] = L;
         so[1] = a0;
-        so[2] = a1;
-        so[3] = a2;
+        so[2] = 0;
+        so[3] = 0;
         so[4] = 0;
         so[5] = 0;
         so[6] = a3;
@@ -812,7 +494,7 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
   const bool walker = wave == 0 && (nbest ? (lane < K && sc != kNegInf) : (lane == 0 && have));
   if (have && L > 0) {
     uint32_t* stg = reinterpret_cast<uint32_t*>(s_big);
-    const int tile_frames = (kBigU64 * 2) / K;
+    const int tile_frames = (kStage * 2) / K;
     int jb = nbest ? lane : best, cnext = -1, pos = 0;
     int32_t* orow = nullptr;
     if (walker) {
@@ -853,25 +535,24 @@ __global__ void __launch_bounds__(kST) small_kernel(KernelParams p) {
   }
 }
 
-template <int NL>
-hipError_t launch_nl(const KernelParams& p, hipStream_t s) {
-  hipLaunchKernelGGL((small_kernel<NL>), dim3(p.B), dim3(kST), 0, s, p);
+hipError_t launch(const KernelParams& p, hipStream_t s) {
+  hipLaunchKernelGGL(small_kernel, dim3(p.B), dim3(kST), 0, s, p);
   return hipGetLastError();
 }
 
 }  // namespace small
 
-// The small-beam decoder is taken where it is faster than the general one:
-// beams of at most 8 without an LM or boosting (1.45 vs 1.72 ms at K = 8 and
-// 1.25 vs 1.67 ms at K = 4 on 32 utterances of 400 frames, V = 1024).  With
-// an LM its rows and single-wave update lose to the general decoder (2.46 vs
-// 2.07 ms on the 3-gram workload at K = 8), so those forms are not built.
+// The small-beam decoder serves beams of at most 8 without an LM or boosting,
+// where it is faster than the general one (1.45 vs 1.72 ms at K = 8 and 1.25
+// vs 1.67 ms at K = 4 on 32 utterances of 400 frames, V = 1024).  A form with
+// LM rows kept in LDS and the update in one wave lost to the general decoder
+// (2.46 vs 2.07 ms on the 3-gram workload at K = 8) and was removed.
 bool small_beam_eligible(const KernelParams& p) {
   if (p.bt_nodes != nullptr || p.lm_states != nullptr || p.lm_arcs != nullptr) return false;
   if (p.K > small::kKmax || p.V > small::kVmax) return false;
   return (p.flags & (kFlagNoRowCache | kFlagLogSumExp | kFlagRepeatScore)) == 0;
 }
 
-hipError_t launch_small(const KernelParams& p, hipStream_t s) { return small::launch_nl<0>(p, s); }
+hipError_t launch_small(const KernelParams& p, hipStream_t s) { return small::launch(p, s); }
 
 }  // namespace ctcbeam
