@@ -176,8 +176,11 @@ __device__ __forceinline__ bool dup_by_sort(uint64_t key, int lane, uint32_t& lo
 // 2^23): LM key rows are kept per LM state across frames and only the states
 // new to the rows are filled; an entry holds its arc's target state.
 // REP: the repeat-scoring variant (CTCBEAM_FLAG_REPEAT_SCORE), a kernel of
-// its own so that the default kernels carry none of its state.
-template <int LPT, int NLEV, bool HAS_BT, int SPL, bool SKIP, bool CACHE, bool REP>
+// its own so that the default kernels carry none of its state.  TREE (beams
+// of 33..64): pools of more than 192 entries are reduced to their top 64 by
+// a merge tree instead of the block rank (a kernel of its own: the code
+// costs the smaller beams' kernels about 3 % through register allocation).
+template <int LPT, int NLEV, bool HAS_BT, int SPL, bool SKIP, bool CACHE, bool REP, bool TREE>
 __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   constexpr bool HAS_LM = NLEV >= 0;
   constexpr int NL = NLEV > 0 ? NLEV : 0;     // chain levels above the unigram root
@@ -249,6 +252,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   __shared__ float s_top[kWaves * 8 * SPL + kWaves];
   __shared__ uint64_t s_red[2][kWaves];
   __shared__ int32_t s_nbuf, s_overflow;
+  // top 64 of a large pool (one slot per lane, beams over one chunk): the
+  // sorted lists of the merge tree (4 + 2 + 1 lists of 64 (lo, hi, source)
+  // triples) and the waves' counts of finite entries
+  constexpr bool kTreeRank = SPL == 1 && SKIP && TREE;
+  __shared__ uint32_t s_srt[kTreeRank ? 7 : 1][3][64];
+  __shared__ int32_t s_wcnt[kWaves];
   __shared__ int32_t s_best, s_bestlen;
   __shared__ float s_bestscore;
   // statistics (only with p.stats): alive beam-frames, LM chain states and
@@ -1205,6 +1214,73 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               s_res[Q][myrank] = make_uint4(eq.x, eq.y, lmt, eq.w);
               if (rep) s_rinc[Q][myrank] = (lane < K) ? s_rinc[P][lane] : s_pinc[lane - K];
             }
+          } else if (kTreeRank && N > 192 && N <= kThreads) {
+            // K <= 64 of 193..512 entries (a few blocks of 64 are cheaper to
+            // rank against each other): each wave sorts its 64 entries by
+            // (score desc, index asc) as 64-bit keys, then a tree of pairwise
+            // merges keeps the top 64 (the 64 largest of two ascending lists
+            // are the elementwise maximum of one and the other reversed, a
+            // bitonic sequence), instead of ranking every entry against
+            // every other
+            const int q = tid;
+            uint4 eq = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+            if (q < N) eq = (q < K) ? s_res[P][q] : s_pool[q - K];
+            const float xq = __uint_as_float(eq.x);
+            const uint64_t key = xq != kNegInf ? order_key(xq, eq.y) : 0ull;
+            uint32_t klo = static_cast<uint32_t>(key), khi = static_cast<uint32_t>(key >> 32);
+            uint32_t ksl = static_cast<uint32_t>(q);
+            sort3_levels<2>(klo, khi, ksl, lane);  // ascending over the wave
+            const int wcnt = __popcll(__ballot(xq != kNegInf));
+            if (lane == 0) s_wcnt[wave] = wcnt;
+            const auto publish = [&](int r) __attribute__((always_inline)) {
+              s_srt[r][0][lane] = klo;
+              s_srt[r][1][lane] = khi;
+              s_srt[r][2][lane] = ksl;
+            };
+            const auto merge_with = [&](int r) __attribute__((always_inline)) {
+              const uint32_t olo = s_srt[r][0][63 - lane], ohi = s_srt[r][1][63 - lane];
+              const uint32_t osl = s_srt[r][2][63 - lane];
+              const bool gt = ohi > khi || (ohi == khi && (olo > klo || (olo == klo && osl > ksl)));
+              klo = gt ? olo : klo;
+              khi = gt ? ohi : khi;
+              ksl = gt ? osl : ksl;
+              sort3_merge<64, 32>(klo, khi, ksl, lane);
+            };
+            if (wave & 1) publish(wave >> 1);  // waves 1, 3, 5, 7: lists 0..3
+            __syncthreads();
+            nfin = 0;
+#pragma unroll
+            for (int w = 0; w < kWaves; ++w) nfin += s_wcnt[w];
+            if ((wave & 1) == 0) merge_with(wave >> 1);
+            if ((wave & 3) == 2) publish(4 + (wave >> 2));  // waves 2, 6: lists 4, 5
+            __syncthreads();
+            if ((wave & 3) == 0) merge_with(4 + (wave >> 2));
+            if (wave == 4) publish(6);
+            __syncthreads();
+            if (wave == 0) {
+              merge_with(6);
+              // lane 63 holds the best entry: rank 63 - lane
+              const int rank = 63 - lane;
+              if (rank < min(K, nfin)) {
+                const uint32_t qq = ksl;
+                const uint4 e = (qq < static_cast<uint32_t>(K)) ? s_res[P][qq] : s_pool[qq - K];
+                uint32_t lmt = e.z;
+                if (HAS_LM && !SKIP && !CACHE && qq >= static_cast<uint32_t>(K)) lmt = lm_target(lmt);
+                s_res[Q][rank] = make_uint4(e.x, e.y, lmt, e.w);
+                if (rep) s_rinc[Q][rank] = (qq < static_cast<uint32_t>(K)) ? s_rinc[P][qq] : s_pinc[qq - K];
+              }
+            }
+            if (last_chunk) {
+              __syncthreads();  // region Q complete
+              const bool act = wave == 0 && tid < min(K, nfin);
+              uint4 e = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
+              if (act) e = s_res[Q][tid];
+              Succ sp;
+              succ_begin(act, e.y, e.z, e.w, prec, sp);
+              succ_end(sp, e.x);
+              if (act) store_rec(nrec + tid * RW, sp.r);
+              if (rep && act && sp.emit) put_terms(nrec + tid * RW, s_rinc[Q][tid]);
+            }
           } else {
             // blocks of 64 entries: this wave ranks entries qb + (wave + 8u)
             // against every entry, lane f holding entry fb + f
@@ -2146,27 +2222,36 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   }
 }
 
-template <int LPT, int NLEV, int SPL, bool SKIP, bool REP>
-hipError_t launch_skip(const KernelParams& p, hipStream_t s) {
+template <int LPT, int NLEV, int SPL, bool SKIP, bool REP, bool TREE>
+hipError_t launch_tree(const KernelParams& p, hipStream_t s) {
   dim3 grid(p.B), block(kThreads);
   constexpr bool kCacheable = SPL == 1 && !SKIP && LPT >= 2 && NLEV > 0;
   if constexpr (REP) {
     // the repeat-scoring variant reads uncached rows; with neither an LM nor
     // boosting it has nothing to repeat (the caller takes the default kernel)
     if (p.bt_nodes != nullptr) {
-      hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP, false, true>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP, false, true, TREE>), grid, block, 0, s, p);
     } else {
       if constexpr (NLEV < 0) return hipErrorInvalidValue;
-      else hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, false, true>), grid, block, 0, s, p);
+      else hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, false, true, TREE>), grid, block, 0, s, p);
     }
   } else if (p.bt_nodes != nullptr) {
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP, false, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, true, SPL, SKIP, false, false, TREE>), grid, block, 0, s, p);
   } else if (kCacheable && p.lm_states_below_2p23 && !(p.flags & kFlagNoRowCache)) {
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, kCacheable, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, kCacheable, false, TREE>), grid, block, 0, s, p);
   } else {
-    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, false, false>), grid, block, 0, s, p);
+    hipLaunchKernelGGL((decode_kernel<LPT, NLEV, false, SPL, SKIP, false, false, TREE>), grid, block, 0, s, p);
   }
   return hipGetLastError();
+}
+
+template <int LPT, int NLEV, int SPL, bool SKIP, bool REP>
+hipError_t launch_skip(const KernelParams& p, hipStream_t s) {
+  // the merge-tree rank for beams of 33..64 over several chunks
+  if constexpr (SPL == 1 && SKIP) {
+    if (p.K > 32) return launch_tree<LPT, NLEV, SPL, SKIP, REP, true>(p, s);
+  }
+  return launch_tree<LPT, NLEV, SPL, SKIP, REP, false>(p, s);
 }
 
 template <int LPT, int NLEV, int SPL, bool REP>
