@@ -109,8 +109,8 @@ def _usable_cores() -> int:
 
 
 def cpu_baseline(w, lp, lens, threads: int, mode: str = "beam", reps: int = 5):
-    """The CPU oracle on the host cores, timed as the survey's protocol asks:
-    one warm-up run, then the median of ``reps`` runs, (i) on one thread over
+    """The CPU oracle on the host cores, timed as one warm-up run, then the
+    median of ``reps`` runs, (i) on one thread over
     one utterance and (ii) on ``threads`` threads over ``threads`` utterances
     (one per thread), wall time by time.perf_counter.  Frames/s counts padded
     frames (B*T), like the GPU metric."""
@@ -171,8 +171,9 @@ def main():
                          "(calibrates rocprofv3 FETCH_SIZE/WRITE_SIZE against known bytes)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the "
-              "decoder shards utterances across GPUs only in design, see DESIGN.md", file=sys.stderr)
+        print(f"bench.py: measures one GPU (asked for --gpus {args.gpus}); the decoder's utterances "
+              "are independent and would be dealt across GPUs one shard each, which is not "
+              "implemented", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
