@@ -54,7 +54,7 @@ extern "C" {
 typedef struct ctcbeam_lm ctcbeam_lm;
 typedef struct ctcbeam_boost ctcbeam_boost;
 
-/* Limits of this build (requests beyond them return 2). */
+/* Limits of the library (requests beyond them return 2). */
 #define CTCBEAM_MAX_K 128       /* beam size (above 64: V <= 1024) */
 #define CTCBEAM_MAX_V 4096      /* tokens (blank excluded) */
 #define CTCBEAM_MAX_ORDER 8     /* n-gram order */
