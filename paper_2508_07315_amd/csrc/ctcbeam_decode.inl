@@ -216,6 +216,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // registers in the scoring.  Shorter chains, and the many chunks of two
   // slots per lane, fold in the scoring: cheaper than the extra LDS maxima.
   constexpr bool kFoldRows = CACHE || (NL >= 4 && SPL == 1);
+  // One slot per lane without the row cache, LMs of order 5 and above:
+  // beams of a chunk that share an LM state share one LM row (the first such
+  // beam's); the others' rows are not filled.  A row's fill walks the
+  // back-off chain, so the saving grows with the order; below order 5 the
+  // extra registers of the sharing cost more than the fills it saves.
+  constexpr bool kDedup = SPL == 1 && !CACHE && HAS_LM && NL >= 4;
   constexpr int kRowWords = kFoldRows ? 4 : 16;  // beam record per live position
   // beam state record (one per slot, double-buffered by frame): score bits,
   // back-pointer, transcript hash (2), length, last label, LM state, then
@@ -321,6 +327,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   uint32_t btb[SPL], btc[SPL];
   int32_t btpot[SPL];
   bool alive[SPL];
+  // LM state of slot j (kDedup): the key of the row sharing
+  uint32_t lmsr = (j == 0) ? p.lm_bos_state : 0xFFFFFFFFu;
 #pragma unroll
   for (int h = 0; h < SPL; ++h) {
     sc[h] = (h == 0 && j == 0) ? 0.0f : kNegInf;
@@ -546,11 +554,30 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       bool inch[SPL];
       int row[SPL];
       int kc = 0;
+      // kDedup: the chunk row whose LM row this beam reads (the lowest one
+      // with the same LM state), and whether it is that row's beam
+      int lrow = 0;
+      bool lfirst = true;
       if constexpr (SPL == 1) {
         inch[0] = alive[0] && (cid[0] == ch);
         const uint64_t chmask = __ballot(inch[0]);
         kc = __popcll(chmask);
         row[0] = __popcll(chmask & lmlt);
+        if constexpr (kDedup) {
+          lrow = row[0];
+          bool found = false;
+          for (uint64_t mm = chmask; mm != 0ull; mm &= mm - 1ull) {  // members in row order
+            const int jm = static_cast<int>(__builtin_ctzll(mm));
+            const bool same = !found && rdlane(lmsr, jm) == lmsr;
+            lrow = same ? rdlane(row[0], jm) : lrow;
+            found = found || same;
+          }
+          lfirst = lrow == row[0];
+          // the row table's slot field carries the LM row (wave 2 wrote the
+          // record in the update; the candidates read it after barrier A)
+          if (wave == 2 && inch[0])
+            s_row[(cs + row[0]) * kRowWords + 2] = static_cast<uint32_t>(j) | (static_cast<uint32_t>(lrow) << 8);
+        }
       } else {
 #pragma unroll
         for (int h = 0; h < SPL; ++h) {
@@ -585,7 +612,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         for (int l = 0; l < NL; ++l) {
 #pragma unroll
           for (int h = 0; h < SPL; ++h) {
-            const uint32_t n = (CACHE ? fillrep : inch[h]) ? (lvc[h][l] & ~kExists) : 0u;
+            const uint32_t n = (CACHE ? fillrep : (inch[h] && lfirst)) ? (lvc[h][l] & ~kExists) : 0u;
             const uint64_t m = __ballot(n != 0u);
             const int nl = __popcll(m);
             if (nl > 0) {  // wave-uniform
@@ -622,7 +649,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           // the explicit arcs (order >= 1) win the maximum
 #pragma unroll
           for (int h = 0; h < SPL; ++h) {
-            uint64_t fm = __ballot(inch[h]);
+            uint64_t fm = __ballot(inch[h] && lfirst);
             while (fm != 0ull) {  // uniform
               const int jr = static_cast<int>(__builtin_ctzll(fm));
               fm &= fm - 1ull;
@@ -795,8 +822,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         const uint4 h0 = *reinterpret_cast<const uint4*>(rr);
         ksc[i] = (i < kc) ? __uint_as_float(h0.x) : kNegInf;
         klast[i] = static_cast<int>(h0.y);
-        kslot[i] = static_cast<int>(CACHE ? (h0.z & 0xFFu) : h0.z);
-        krow[i] = CACHE ? ((h0.z >> 8) & 0xFFu) : static_cast<uint32_t>(i);
+        kslot[i] = static_cast<int>((CACHE || kDedup) ? (h0.z & 0xFFu) : h0.z);
+        krow[i] = (CACHE || kDedup) ? ((h0.z >> 8) & 0xFFu) : static_cast<uint32_t>(i);
         kpot[i] = static_cast<int>(h0.w);
 #pragma unroll
         for (int l0 = 0; l0 < (kFoldRows ? 0 : NL); l0 += 4) {
@@ -821,6 +848,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const int r = i * LPT + jj;
           const int c = tid + jj * kThreads;
           const uint32_t e = static_cast<uint32_t>(i * V) + rcc[jj];
+          // LM entry: the row this beam reads (shared with its state's first beam)
+          const uint32_t el = kDedup ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
           const float x0 = ksc[i] + rD[jj];
           float x1 = x0 + beta;
           if (HAS_LM) {
@@ -833,11 +862,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             } else if constexpr (kFoldRows) {
               // the chunk's rows hold every token: the fold (order 0, the
               // token) or an explicit arc (its staging slot, resolved later)
-              const uint64_t ent = lmrow[e];
+              const uint64_t ent = lmrow[el];
               x1 = x1 + __uint_as_float(static_cast<uint32_t>(ent));
               if constexpr (kKeepLm) lhi[r] = static_cast<uint32_t>(ent >> 32);
             } else {
-              const uint64_t ent = lmrow[e];
+              const uint64_t ent = lmrow[el];
               const uint32_t hi = static_cast<uint32_t>(ent >> 32);
               float v = rP1[jj];
 #pragma unroll
@@ -899,9 +928,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           if constexpr (CACHE) {
             av = __uint_as_float(static_cast<uint32_t>(lmrow[row * static_cast<uint32_t>(V) + c]));
           } else if constexpr (kFoldRows) {
-            av = __uint_as_float(static_cast<uint32_t>(lmrow[e]));
+            const uint32_t el = kDedup ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
+            av = __uint_as_float(static_cast<uint32_t>(lmrow[el]));
           } else {
-            const uint64_t ent = lmrow[e];
+            const uint32_t el = kDedup ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
+            const uint64_t ent = lmrow[el];
             if (static_cast<uint32_t>(ent >> 32) >= genhi) {
               av = __uint_as_float(static_cast<uint32_t>(ent));
             } else {
@@ -927,7 +958,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 #pragma unroll 1
         for (int q = 0; q < kc; ++q) {
           const uint32_t z = s_row[(cs + q) * kRowWords + 2];
-          if ((CACHE ? (z & 0xFFu) : z) == slot) {
+          if (((CACHE || kDedup) ? (z & 0xFFu) : z) == slot) {
             i = static_cast<uint32_t>(q);
             row = (z >> 8) & 0xFFu;
           }
@@ -945,7 +976,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           if constexpr (CACHE) {
             lraw = static_cast<uint32_t>(lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]] >> 32) & kTargetMask;
           } else {
-            const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
+            const uint32_t el = kDedup ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
+            const uint32_t hi = static_cast<uint32_t>(lmrow[el] >> 32);
             lraw = (kFoldRows || hi >= genhi) ? hi : rcc[jj];
           }
         }
@@ -1365,7 +1397,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   wflat = flat;
                   wi = static_cast<uint32_t>(i);
                   wjj = static_cast<uint32_t>(jj);
-                  if constexpr (CACHE) wrow = krow[i];
+                  if constexpr (CACHE || kDedup) wrow = krow[i];
                 }
               }
             }
@@ -1412,7 +1444,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   if constexpr (CACHE) {
                     lmt = static_cast<uint32_t>(lmrow[wrow * static_cast<uint32_t>(V) + c] >> 32) & kTargetMask;
                   } else {
-                    const uint32_t hi = static_cast<uint32_t>(lmrow[e] >> 32);
+                    const uint32_t el = kDedup ? wrow * static_cast<uint32_t>(V) + c : e;
+                    const uint32_t hi = static_cast<uint32_t>(lmrow[el] >> 32);
                     lmt = (kFoldRows || hi >= genhi) ? lm_target(hi) : c;
                   }
                 }
@@ -1547,6 +1580,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       last[0] = nlast;
       len[0] = nlen;
       alive[0] = nalive;
+      if constexpr (kDedup) lmsr = nalive ? rec[kRLms] : 0xFFFFFFFFu;
       int32_t acnt = 0;
 #pragma unroll
       for (int l = 0; l < NL; ++l) {

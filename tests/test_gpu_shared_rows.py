@@ -1,0 +1,142 @@
+"""GPU parity of shared LM rows: with a 5-gram or higher-order LM, no row
+cache and one beam slot per lane, beams of one chunk that sit in the same LM
+state read one LM row (filled once) instead of one row each.  Sharing
+changes which rows are filled, never a score, so the results must equal the
+CPU oracle's (tokens bit-exact, scores within 1e-4).
+
+* 5- and 6-gram LMs of a few thousand n-grams (most hypotheses back off to
+  short, shared states) with K = 9..64, vocabularies of 300, 1024 and 1500
+  tokens (one, two and four labels per lane), with and without boosting,
+  theta = inf and 12, 1-best and N-best;
+* log-sum-exp recombination and repeat scoring on the same path;
+* a witness that the final beams do share LM states (the longest suffix of
+  <s> + tokens that is an n-gram of the model), so that the shared-row path
+  is the one these cases run.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2508_07315_amd as P
+import workloads as W
+from gpu_helpers import compare, device, handles, log, oracle_threads
+
+pytestmark = pytest.mark.gpu
+
+
+def _workload(order, V, K, boost, seed):
+    counts = tuple([min(3 * V, (V + 1) ** 2)] + [2 * V] * (order - 2))
+    return W.CONFIGS[6].replace(
+        B=3, T=90, V=V, K=K, lengths=("uniform", 40, 90), seed=seed,
+        lm=W.LMSpec(order=order, counts=counts, seed=seed + 1),
+        boost=W.BoostSpec(300, 2, 5, "uniform", seed + 2) if boost else None,
+        boost_w=1.5 if boost else 0.0)
+
+
+def _run(lp, lens, K, w, lm, bt, theta, nbest=False, **kw):
+    import torch
+    dev = device()
+    d_lp = torch.from_numpy(np.ascontiguousarray(lp)).to(dev)
+    d_len = torch.from_numpy(np.ascontiguousarray(lens, dtype=np.int32)).to(dev)
+    f = P.ctcbeam_decode_nbest if nbest else P.ctcbeam_decode_ex
+    tok, ln, sc, ws = f(d_lp, d_len, K, w.alpha, w.beta, w.boost_w, lm, bt, theta=theta, **kw)
+    torch.cuda.synchronize()
+    return dict(tokens=tok.cpu().numpy(), lengths=ln.cpu().numpy(), scores=sc.cpu().numpy(),
+                status=P.ctcbeam_query_status(ws))
+
+
+def _compare_nbest(g, r, what):
+    np.testing.assert_array_equal(g["lengths"], r["nbest_lengths"], err_msg=what)
+    np.testing.assert_array_equal(g["tokens"], r["nbest_tokens"], err_msg=what)
+    gs, rs = g["scores"], r["nbest_scores"]
+    inf = np.isinf(gs) | np.isinf(rs)
+    np.testing.assert_array_equal(gs[inf], rs[inf], err_msg=what)
+    assert np.all(np.abs(gs[~inf].astype(np.float64) - rs[~inf]) <= 1e-4), what
+
+
+def _lm_state(entries, order, bos, toks):
+    """Longest suffix of <s> + toks, at most order-1 long, that is an n-gram."""
+    y = (bos,) + tuple(int(t) for t in toks)
+    for L in range(min(order - 1, len(y)), 0, -1):
+        if y[-L:] in entries[L - 1]:
+            return y[-L:]
+    return ()
+
+
+@pytest.mark.parametrize("order,V,K,boost", [
+    (5, 1024, 16, False), (5, 1024, 64, True), (6, 1024, 40, True), (6, 1024, 64, False),
+    (6, 1024, 9, True), (6, 300, 33, True), (5, 1500, 64, False), (5, 1500, 24, True)])
+def test_shared_rows(order, V, K, boost):
+    w = _workload(order, V, K, boost, 31000 + 97 * order + K)
+    lm, bt, olm, obt = handles(w)
+    lp = W.make_logprobs(w)
+    lens = W.make_lengths(w)
+    for th in (math.inf, 12.0):
+        log(f"shared rows order={order} V={V} K={K} boost={boost} theta={th}")
+        r = oracle.decode(lp, lens, K, w.alpha, w.beta, w.boost_w, theta=th, lm=olm, bt=obt,
+                          n_threads=oracle_threads(), want_nbest=True)
+        g = _run(lp, lens, K, w, lm, bt, th)
+        assert g["status"] == 0
+        compare(g, r, what=f"order={order} V={V} K={K} boost={boost} theta={th}")
+        gn = _run(lp, lens, K, w, lm, bt, th, nbest=True)
+        _compare_nbest(gn, r, what=f"nbest order={order} V={V} K={K} theta={th}")
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_shared_rows_random_logits(seed):
+    # flat logits keep many distinct hypotheses alive
+    rng = np.random.default_rng(32000 + seed)
+    V = int(rng.choice([200, 700, 1024]))
+    order = int(rng.integers(5, 8 if V <= 500 else 7))  # LM ids need (V+2)^order < 2^62
+    K = int(rng.integers(9, 65))
+    w = _workload(order, V, K, bool(rng.random() < 0.5), 32100 + seed)
+    lm, bt, olm, obt = handles(w)
+    B, T = 2, int(rng.integers(20, 70))
+    lens = rng.integers(0, T + 1, size=B)
+    lens[0] = T
+    lp = W.random_logprobs(rng, B, T, V, scale=float(rng.uniform(0.5, 2.5)))
+    lse = bool(rng.random() < 0.5)
+    log(f"shared rows fuzz {seed}: order={order} V={V} K={K} T={T} lse={lse}")
+    r = oracle.decode(lp, lens, K, w.alpha, w.beta, w.boost_w, lm=olm, bt=obt,
+                      n_threads=oracle_threads(), want_nbest=True, logsumexp=lse)
+    gn = _run(lp, lens, K, w, lm, bt, math.inf, nbest=True, logsumexp=lse)
+    assert gn["status"] == 0
+    _compare_nbest(gn, r, what=f"fuzz {seed}")
+
+
+@pytest.mark.parametrize("boost", [False, True])
+def test_shared_rows_repeat_score(boost):
+    w = _workload(6, 1024, 32, boost, 33000 + int(boost))
+    lm, bt, olm, obt = handles(w)
+    lp = W.make_logprobs(w)
+    lens = W.make_lengths(w)
+    log(f"shared rows repeat scoring boost={boost}")
+    r = oracle.decode(lp, lens, w.K, w.alpha, w.beta, w.boost_w, lm=olm, bt=obt,
+                      n_threads=oracle_threads(), want_nbest=True, repeat_score=True)
+    g = _run(lp, lens, w.K, w, lm, bt, math.inf, repeat_score=True)
+    compare(g, r, what=f"repeat boost={boost}")
+    gn = _run(lp, lens, w.K, w, lm, bt, math.inf, nbest=True, repeat_score=True)
+    _compare_nbest(gn, r, what=f"repeat nbest boost={boost}")
+
+
+def test_final_beams_share_lm_states():
+    w = _workload(6, 1024, 64, False, 34000)
+    lm, _, olm, _ = handles(w)
+    lp = W.make_logprobs(w)
+    lens = W.make_lengths(w)
+    gn = _run(lp, lens, w.K, w, lm, None, math.inf, nbest=True)
+    arrays = W.lm_for(w.lm, w.V)
+    entries = [set(map(tuple, ids.tolist())) for ids in arrays["ids"][: w.lm.order - 1]]
+    shared = 0
+    for b in range(w.B):
+        live = [r for r in range(w.K) if gn["scores"][b, r] != -np.inf]
+        states = {_lm_state(entries, w.lm.order, w.V + 1, gn["tokens"][b, r, : gn["lengths"][b, r]])
+                  for r in live}
+        log(f"utterance {b}: {len(live)} beams, {len(states)} LM states")
+        shared += len(live) - len(states)
+    assert shared > 0
+    r = oracle.decode(lp, lens, w.K, w.alpha, w.beta, 0.0, lm=olm, n_threads=oracle_threads(),
+                      want_nbest=True)
+    _compare_nbest(gn, r, what="witness workload")
