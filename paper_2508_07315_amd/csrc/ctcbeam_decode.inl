@@ -221,7 +221,15 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // beam's); the others' rows are not filled.  A row's fill walks the
   // back-off chain, so the saving grows with the order; below order 5 the
   // extra registers of the sharing cost more than the fills it saves.
-  constexpr bool kDedup = SPL == 1 && !CACHE && HAS_LM && NL >= 4;
+  // Fill groups (one slot per lane, beams over one chunk, no row cache): the
+  // update orders the live beams by LM state and, within a state, by
+  // boosting list, and cuts that order into groups of consecutive chunks
+  // whose distinct LM states (at most KSEG), boosting lists (at most KCR)
+  // and staged arcs (at most kLmStage) fit the rows.  A state or list has one
+  // row per group, filled at the group's first chunk; the group's other
+  // chunks skip the fill and its barrier.
+  constexpr bool kGroups = SPL == 1 && !CACHE && SKIP && (HAS_LM || HAS_BT);
+  constexpr bool kDedup = SPL == 1 && !CACHE && !kGroups && HAS_LM && NL >= 4;
   constexpr int kRowWords = kFoldRows ? 4 : 16;  // beam record per live position
   // beam state record (one per slot, double-buffered by frame): score bits,
   // back-pointer, transcript hash (2), length, last label, LM state, then
@@ -288,6 +296,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   const int b = blockIdx.x;
   const int V = p.V, W = V + 1, K = p.K, T = p.T;
   const int kcmax = min(K, KSEG);
+  const int kcg = min(K, KCR);  // beams per chunk with fill groups
   const float alpha = p.alpha, beta = p.beta, boost_w = p.boost_w;
   const uint64_t lmlt = lanemask_lt();
   // repeat-scoring variant: a repeated token gets its LM / boosting terms again
@@ -329,6 +338,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   bool alive[SPL];
   // LM state of slot j (kDedup): the key of the row sharing
   uint32_t lmsr = (j == 0) ? p.lm_bos_state : 0xFFFFFFFFu;
+  // kGroups: fill group of slot j (-1: dead), its LM and boosting rows there
+  // and whether slot j fills them; lane q: the first chunk of group q
+  int grp = 0, lrow_g = 0, brow_g = 0;
+  bool lown = j == 0, bown = j == 0;
+  int gch0 = 0, ngrp = 1;
 #pragma unroll
   for (int h = 0; h < SPL; ++h) {
     sc[h] = (h == 0 && j == 0) ? 0.0f : kNegInf;
@@ -384,7 +398,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // (bits 8..15)
   auto put_row = [&](int lp, int h) __attribute__((always_inline)) {
     uint32_t* rr = s_row + lp * kRowWords;
-    const uint32_t zf = static_cast<uint32_t>(j + 64 * h) | (CACHE ? static_cast<uint32_t>(rowof) << 8 : 0u);
+    uint32_t zf = static_cast<uint32_t>(j + 64 * h) | (CACHE ? static_cast<uint32_t>(rowof) << 8 : 0u);
+    if constexpr (kGroups) zf |= (static_cast<uint32_t>(lrow_g) << 8) | (static_cast<uint32_t>(brow_g) << 16);
     *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc[h]), static_cast<uint32_t>(last[h]),
                                                zf, static_cast<uint32_t>(btpot[h]));
 #pragma unroll
@@ -548,6 +563,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     // survivors carried in the pool from chunks whose rank was skipped
     int carry = 0;
     int cs = 0;  // live position of the chunk's first beam
+    int gi = 0;  // next fill group (kGroups)
 
     for (int ch = 0; ch < nch; ++ch) {
       // this chunk's beams and their key rows (slot order)
@@ -588,15 +604,39 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         }
       }
 
-      // ---- F. fill the key rows of this chunk ----
-      if (gen == kGenMax) {
-        // rows were last read before the previous filter barrier
-        for (int i = tid; i < kOffTgt; i += kThreads) s_big[i] = 0u;
-        __syncthreads();
-        gen = 0u;
+      // ---- F. fill the key rows of this chunk (of its group) ----
+      // kGroups: only a group's first chunk fills (uniform)
+      const bool gfill = !kGroups || (gi < ngrp && ch == rdlane(gch0, gi));
+      // the fill's beams: slots that fill an LM row / a boosting row, and the rows
+      const auto lm_sel = [&](int h) __attribute__((always_inline)) {
+        if constexpr (CACHE) return fillrep;
+        else if constexpr (kGroups) return alive[h] && grp == gi && lown;
+        else return inch[h] && lfirst;
+      };
+      const auto lm_rowof = [&](int h) __attribute__((always_inline)) {
+        if constexpr (CACHE) return rowof;
+        else if constexpr (kGroups) return lrow_g;
+        else return row[h];
+      };
+      const auto bt_sel = [&](int h) __attribute__((always_inline)) {
+        if constexpr (kGroups) return alive[h] && grp == gi && bown;
+        else return inch[h];
+      };
+      const auto bt_rowof = [&](int h) __attribute__((always_inline)) {
+        if constexpr (kGroups) return brow_g;
+        else return row[h];
+      };
+      if (gfill) {  // uniform
+        if (gen == kGenMax) {
+          // rows were last read before the previous filter barrier
+          for (int i = tid; i < kOffTgt; i += kThreads) s_big[i] = 0u;
+          __syncthreads();
+          gen = 0u;
+        }
+        ++gen;
       }
-      ++gen;
       const uint32_t genhi = gen << kGenShift;
+      if (gfill) {  // uniform
       if (HAS_LM && NL > 0) {
         // Segment table, lane s = segment s: the non-empty (beam, level) arc
         // runs of the chunk, level-major.  The chunk's arcs are numbered by
@@ -612,7 +652,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         for (int l = 0; l < NL; ++l) {
 #pragma unroll
           for (int h = 0; h < SPL; ++h) {
-            const uint32_t n = (CACHE ? fillrep : (inch[h] && lfirst)) ? (lvc[h][l] & ~kExists) : 0u;
+            const uint32_t n = lm_sel(h) ? (lvc[h][l] & ~kExists) : 0u;
             const uint64_t m = __ballot(n != 0u);
             const int nl = __popcll(m);
             if (nl > 0) {  // wave-uniform
@@ -624,7 +664,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               const uint32_t r_base =
                   static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(lvb[h][l])));
               const uint32_t r_rl =
-                  static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, (CACHE ? rowof : row[h]) | (l << 8)));
+                  static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, lm_rowof(h) | (l << 8)));
               float r_f[NF];
 #pragma unroll
               for (int k = 0; k + 1 < NL; ++k) {
@@ -649,11 +689,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           // the explicit arcs (order >= 1) win the maximum
 #pragma unroll
           for (int h = 0; h < SPL; ++h) {
-            uint64_t fm = __ballot(inch[h] && lfirst);
+            uint64_t fm = __ballot(lm_sel(h));
             while (fm != 0ull) {  // uniform
               const int jr = static_cast<int>(__builtin_ctzll(fm));
               fm &= fm - 1ull;
-              const uint32_t rf = rdlane(static_cast<uint32_t>(row[h]), jr);
+              const uint32_t rf = rdlane(static_cast<uint32_t>(lm_rowof(h)), jr);
               float bo[NLA];
 #pragma unroll
               for (int l = 0; l < NL; ++l) bo[l] = rdlane(lvbo[h][l], jr);
@@ -755,7 +795,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         uint32_t bg_cnt = 0u, bg_base = 0u, bg_row = 0u;
 #pragma unroll
         for (int h = 0; h < SPL; ++h) {
-          const uint32_t nb = inch[h] ? btc[h] : 0u;
+          const uint32_t nb = bt_sel(h) ? btc[h] : 0u;
           const uint64_t m = __ballot(nb != 0u);
           const int nl = __popcll(m);
           if (nl > 0) {  // wave-uniform
@@ -763,7 +803,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             const int addr = dst << 2;
             const uint32_t r_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(nb)));
             const uint32_t r_base = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(btb[h])));
-            const uint32_t r_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, row[h]));
+            const uint32_t r_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, bt_rowof(h)));
             if (lane >= S && lane < S + nl) {
               bg_cnt = r_cnt;
               bg_base = r_base;
@@ -805,6 +845,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       CTCBEAM_PHASE_MARK(0);
       __syncthreads();  // A: rows complete
       CTCBEAM_PHASE_MARK(1);
+      if constexpr (kGroups) ++gi;
+      }
 
       // ---- C. candidates ----
       // chunk row i is live position cs + i; its beam record is read with
@@ -814,16 +856,19 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       int klast[KCR];
       float kbo[KCR][NLA];  // backoff weights (rows without the fold)
       int kpot[KCR];
-      // LM key row of chunk row i
-      uint32_t krow[KCR];
+      // LM key row and boosting row of chunk row i
+      uint32_t krow[KCR], kbrow[KCR];
 #pragma unroll
       for (int i = 0; i < KCR; ++i) {
         const uint32_t* rr = s_row + (cs + i) * kRowWords;
         const uint4 h0 = *reinterpret_cast<const uint4*>(rr);
         ksc[i] = (i < kc) ? __uint_as_float(h0.x) : kNegInf;
         klast[i] = static_cast<int>(h0.y);
-        kslot[i] = static_cast<int>((CACHE || kDedup) ? (h0.z & 0xFFu) : h0.z);
-        krow[i] = (CACHE || kDedup) ? ((h0.z >> 8) & 0xFFu) : static_cast<uint32_t>(i);
+        // (uniform: fill groups keep the fields in scalar registers)
+        const uint32_t hz = kGroups ? __builtin_amdgcn_readfirstlane(h0.z) : h0.z;
+        kslot[i] = static_cast<int>((CACHE || kDedup || kGroups) ? (hz & 0xFFu) : hz);
+        krow[i] = (CACHE || kDedup || kGroups) ? ((hz >> 8) & 0xFFu) : static_cast<uint32_t>(i);
+        kbrow[i] = kGroups ? ((hz >> 16) & 0xFFu) : static_cast<uint32_t>(i);
         kpot[i] = static_cast<int>(h0.w);
 #pragma unroll
         for (int l0 = 0; l0 < (kFoldRows ? 0 : NL); l0 += 4) {
@@ -849,7 +894,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const int c = tid + jj * kThreads;
           const uint32_t e = static_cast<uint32_t>(i * V) + rcc[jj];
           // LM entry: the row this beam reads (shared with its state's first beam)
-          const uint32_t el = kDedup ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
+          const uint32_t el = (kDedup || kGroups) ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
           const float x0 = ksc[i] + rD[jj];
           float x1 = x0 + beta;
           if (HAS_LM) {
@@ -880,7 +925,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
           }
           if (HAS_BT) {
-            const uint32_t be = btrow[e];
+            const uint32_t be = btrow[kGroups ? kbrow[i] * static_cast<uint32_t>(V) + rcc[jj] : e];
             const uint32_t bk = (be >= genhi) ? be : rRoot[jj];
             const int pre = static_cast<int>((bk >> 20) & 63u);
             const float bv = boost_w * static_cast<float>(pre - kpot[i]);
@@ -928,10 +973,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           if constexpr (CACHE) {
             av = __uint_as_float(static_cast<uint32_t>(lmrow[row * static_cast<uint32_t>(V) + c]));
           } else if constexpr (kFoldRows) {
-            const uint32_t el = kDedup ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
+            const uint32_t el = (kDedup || kGroups) ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
             av = __uint_as_float(static_cast<uint32_t>(lmrow[el]));
           } else {
-            const uint32_t el = kDedup ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
+            const uint32_t el = (kDedup || kGroups) ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
             const uint64_t ent = lmrow[el];
             if (static_cast<uint32_t>(ent >> 32) >= genhi) {
               av = __uint_as_float(static_cast<uint32_t>(ent));
@@ -944,7 +989,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           }
         }
         if (HAS_BT) {
-          const uint32_t be = btrow[e];
+          const uint32_t be = btrow[kGroups ? ((rr[2] >> 16) & 0xFFu) * static_cast<uint32_t>(V) + c : e];
           const uint32_t bk = (be >= genhi) ? be : p.bt_root_key[c];
           bv = boost_w * static_cast<float>(static_cast<int>((bk >> 20) & 63u) - static_cast<int>(rr[3]));
         }
@@ -958,7 +1003,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 #pragma unroll 1
         for (int q = 0; q < kc; ++q) {
           const uint32_t z = s_row[(cs + q) * kRowWords + 2];
-          if (((CACHE || kDedup) ? (z & 0xFFu) : z) == slot) {
+          if (((CACHE || kDedup || kGroups) ? (z & 0xFFu) : z) == slot) {
             i = static_cast<uint32_t>(q);
             row = (z >> 8) & 0xFFu;
           }
@@ -976,13 +1021,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           if constexpr (CACHE) {
             lraw = static_cast<uint32_t>(lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]] >> 32) & kTargetMask;
           } else {
-            const uint32_t el = kDedup ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
+            const uint32_t el = (kDedup || kGroups) ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
             const uint32_t hi = static_cast<uint32_t>(lmrow[el] >> 32);
             lraw = (kFoldRows || hi >= genhi) ? hi : rcc[jj];
           }
         }
         if (HAS_BT) {
-          const uint32_t be = btrow[e];
+          const uint32_t be = btrow[kGroups ? kbrow[i] * static_cast<uint32_t>(V) + rcc[jj] : e];
           bk = (be >= genhi) ? be : rRoot[jj];
         }
       };
@@ -1382,7 +1427,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             // the best register candidate's fields, tracked by selects so that
             // no candidate array is indexed at run time
             float wx = kNegInf;
-            uint32_t wflat = 0u, wi = 0u, wjj = 0u, wrow = 0u;
+            uint32_t wflat = 0u, wi = 0u, wjj = 0u, wrow = 0u, wbrow = 0u;
 #pragma unroll
             for (int r = 0; r < NC; ++r) {
               if (cand[r] != kNegInf) {
@@ -1397,7 +1442,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   wflat = flat;
                   wi = static_cast<uint32_t>(i);
                   wjj = static_cast<uint32_t>(jj);
-                  if constexpr (CACHE || kDedup) wrow = krow[i];
+                  if constexpr (CACHE || kDedup || kGroups) wrow = krow[i];
+                  if constexpr (kGroups) wbrow = kbrow[i];
                 }
               }
             }
@@ -1444,13 +1490,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   if constexpr (CACHE) {
                     lmt = static_cast<uint32_t>(lmrow[wrow * static_cast<uint32_t>(V) + c] >> 32) & kTargetMask;
                   } else {
-                    const uint32_t el = kDedup ? wrow * static_cast<uint32_t>(V) + c : e;
+                    const uint32_t el = (kDedup || kGroups) ? wrow * static_cast<uint32_t>(V) + c : e;
                     const uint32_t hi = static_cast<uint32_t>(lmrow[el] >> 32);
                     lmt = (kFoldRows || hi >= genhi) ? lm_target(hi) : c;
                   }
                 }
                 if (HAS_BT) {
-                  const uint32_t be = btrow[e];
+                  const uint32_t be = btrow[kGroups ? wbrow * static_cast<uint32_t>(V) + c : e];
                   bk = (be >= genhi) ? be : p.bt_root_key[c];
                 }
                 s_res[Q][it] = make_uint4(__float_as_uint(wx), wflat, lmt, bk);
@@ -1624,7 +1670,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       // live positions and beam records for the next frame
       const uint64_t amask = __ballot(nalive);
       const int na = __popcll(amask);
-      const int lp = __popcll(amask & lmlt);
+      int lp = __popcll(amask & lmlt);
       if constexpr (CACHE) {
         // Key rows of the new beam: a live slot whose LM state has a row
         // keeps it; each other state takes a row no live slot uses (there are
@@ -1678,12 +1724,129 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           mm = __ballot(miss);
         }
       }
+      if constexpr (kGroups) {
+        // Fill groups of the next frame.  LM states are taken in order of
+        // their lowest slot and, within a state, boosting lists in order of
+        // their lowest slot (beams without a list first); a group takes such
+        // (state, list) runs while its rows and staging area have room, and
+        // its beams get consecutive live positions, kcg to a chunk.  A group
+        // holds at most KCR - 1 lists: beams without a list read row KCR - 1,
+        // which the group's fill leaves empty.  Lane q of gch0, gmem and gbl:
+        // the first chunk, the member slots and the list set of group q.
+        const auto rd64 = [&](uint64_t v, int l) __attribute__((always_inline)) {
+          return (static_cast<uint64_t>(rdlane(static_cast<uint32_t>(v >> 32), l)) << 32) |
+                 rdlane(static_cast<uint32_t>(v), l);
+        };
+        const auto bperm64 = [&](uint64_t v, int l) __attribute__((always_inline)) {
+          const int a = l << 2;
+          return (static_cast<uint64_t>(static_cast<uint32_t>(
+                      __builtin_amdgcn_ds_bpermute(a, static_cast<int>(static_cast<uint32_t>(v >> 32)))))
+                  << 32) |
+                 static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(a, static_cast<int>(static_cast<uint32_t>(v))));
+        };
+        const uint32_t lkey = (HAS_LM && NL > 0) ? rec[kRLms] : 0u;  // a unigram LM fills no row
+        // distinct boosting lists (begin, count) of the live beams, numbered
+        // in order of their lowest slot; lane k of bmk: the slots holding list k
+        const bool hasb = HAS_BT && nalive && btc[0] != 0u;
+        const uint64_t hbm = __ballot(hasb);
+        int bidx = 0;
+        uint64_t bmk = 0ull;
+        if constexpr (HAS_BT) {
+          uint64_t brem = hbm;
+          int nbl = 0;
+          while (brem != 0ull) {  // uniform
+            const int jm = static_cast<int>(__builtin_ctzll(brem));
+            const uint32_t b0 = rdlane(btb[0], jm), c0 = rdlane(btc[0], jm);
+            const uint64_t m = __ballot(hasb && btb[0] == b0 && btc[0] == c0);
+            brem &= ~m;
+            if (lane == nbl) bmk = m;
+            if ((m >> j) & 1ull) bidx = nbl;
+            ++nbl;
+          }
+        }
+        uint64_t rem = amask;
+        uint64_t gmem = 0ull, gbl = 0ull;
+        int pos = 0, g = -1, chn = 0;
+        int g_rows = 0, g_arcs = 0, g_beams = 0;
+        uint64_t g_bl = 0ull;
+        gch0 = 0x7FFFFFFF;
+        grp = -1;
+        lown = false;
+        cid[0] = -1;
+        while (rem != 0ull) {  // uniform: one LM state a pass
+          const int js = static_cast<int>(__builtin_ctzll(rem));
+          const uint32_t sk = rdlane(lkey, js);
+          uint64_t smem = __ballot(nalive && lkey == sk);
+          rem &= ~smem;
+          const int a = rdlane(acnt, js);
+          int srow = -1;  // the state's LM row in the current group
+          while (smem != 0ull) {  // uniform: one boosting list a pass
+            const int jb = static_cast<int>(__builtin_ctzll(smem));
+            int kb = -1;
+            uint64_t sub = smem & ~hbm;
+            if (HAS_BT && ((hbm >> jb) & 1ull)) {
+              kb = rdlane(bidx, jb);
+              sub = smem & rd64(bmk, kb);
+            }
+            smem &= ~sub;
+            const bool need_lm = srow < 0;
+            const bool need_bl = kb >= 0 && !((g_bl >> kb) & 1ull);
+            const bool fits = g >= 0 && (!need_lm || (g_rows < KSEG && g_arcs + a <= kLmStage)) &&
+                              (!need_bl || __popcll(g_bl) < KCR - 1);
+            if (!fits) {
+              if (g >= 0) chn += (g_beams + kcg - 1) / kcg;
+              ++g;
+              if (lane == g) gch0 = chn;
+              g_rows = 0;
+              g_arcs = 0;
+              g_beams = 0;
+              g_bl = 0ull;
+              srow = -1;
+              if (a > kLmStage) status |= 4u;  // a single chain above the staging limit (the builders prevent it)
+            }
+            const bool newrow = srow < 0;
+            if (newrow) {
+              srow = g_rows++;
+              g_arcs += a;
+            }
+            if (kb >= 0) g_bl |= 1ull << kb;
+            if ((sub >> j) & 1ull) {
+              const int inq = __popcll(sub & lmlt);
+              lp = pos + inq;
+              cid[0] = chn + (g_beams + inq) / kcg;
+              grp = g;
+              lrow_g = srow;
+              lown = newrow && j == jb;
+            }
+            if (lane == g) {
+              gmem |= sub;
+              gbl = g_bl;
+            }
+            const int cnt = __popcll(sub);
+            g_beams += cnt;
+            pos += cnt;
+          }
+        }
+        if (g >= 0) chn += (g_beams + kcg - 1) / kcg;
+        nch = chn;
+        ngrp = g + 1;
+        if constexpr (HAS_BT) {
+          // list k's row in group q: its rank among the group's lists; the
+          // group's lowest slot holding it fills the row
+          const int gq = max(grp, 0);
+          const uint64_t mg = bperm64(gmem, gq), bg = bperm64(gbl, gq), mk = bperm64(bmk, bidx);
+          brow_g = hasb ? __popcll(bg & ((1ull << bidx) - 1ull)) : KCR - 1;
+          bown = hasb && static_cast<int>(__builtin_ctzll(mk & mg)) == j;
+        }
+      }
       if (wave == 2 && nalive) put_row(lp, 0);
       // chunk plan: live slots in slot order, at most kcmax beams and
       // kLmStage staged arcs per chunk (cached rows stage nothing)
       if constexpr (CACHE) {
         nch = na > 0 ? 1 : 0;  // K <= KCR = kcmax, nothing staged
         cid[0] = 0;
+      } else if constexpr (kGroups) {
+        // planned above
       } else {
       const int ia = wave_incl_scan(acnt, lane);
       const int tota = rdlane(ia, 63);
