@@ -216,20 +216,15 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // registers in the scoring.  Shorter chains, and the many chunks of two
   // slots per lane, fold in the scoring: cheaper than the extra LDS maxima.
   constexpr bool kFoldRows = CACHE || (NL >= 4 && SPL == 1);
-  // One slot per lane without the row cache, LMs of order 5 and above:
-  // beams of a chunk that share an LM state share one LM row (the first such
-  // beam's); the others' rows are not filled.  A row's fill walks the
-  // back-off chain, so the saving grows with the order; below order 5 the
-  // extra registers of the sharing cost more than the fills it saves.
-  // Fill groups (one slot per lane, beams over one chunk, no row cache): the
-  // update orders the live beams by LM state and, within a state, by
-  // boosting list, and cuts that order into groups of consecutive chunks
-  // whose distinct LM states (at most KSEG), boosting lists (at most KCR)
-  // and staged arcs (at most kLmStage) fit the rows.  A state or list has one
-  // row per group, filled at the group's first chunk; the group's other
-  // chunks skip the fill and its barrier.
-  constexpr bool kGroups = SPL == 1 && !CACHE && SKIP && (HAS_LM || HAS_BT);
-  constexpr bool kDedup = SPL == 1 && !CACHE && !kGroups && HAS_LM && NL >= 4;
+  // Fill groups (beams over one chunk, no row cache): the update orders the
+  // live beams by LM state and, within a state, by boosting list, and cuts
+  // that order into groups of consecutive chunks whose distinct LM states
+  // (at most KSEG), boosting lists (at most KCR - 1) and staged arcs (at
+  // most kLmStage) fit the rows.  A state or list has one row per group,
+  // filled at the group's first chunk; the group's other chunks skip the
+  // fill and its barrier.  Large beams hold few distinct states and lists
+  // (at K = 64 about 10 and 6), so a frame fills about two groups.
+  constexpr bool kGroups = !CACHE && SKIP && (HAS_LM || HAS_BT);
   constexpr int kRowWords = kFoldRows ? 4 : 16;  // beam record per live position
   // beam state record (one per slot, double-buffered by frame): score bits,
   // back-pointer, transcript hash (2), length, last label, LM state, then
@@ -336,13 +331,20 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   uint32_t btb[SPL], btc[SPL];
   int32_t btpot[SPL];
   bool alive[SPL];
-  // LM state of slot j (kDedup): the key of the row sharing
-  uint32_t lmsr = (j == 0) ? p.lm_bos_state : 0xFFFFFFFFu;
-  // kGroups: fill group of slot j (-1: dead), its LM and boosting rows there
-  // and whether slot j fills them; lane q: the first chunk of group q
-  int grp = 0, lrow_g = 0, brow_g = 0;
-  bool lown = j == 0, bown = j == 0;
-  int gch0 = 0, ngrp = 1;
+  // kGroups: fill group of slot j + 64 h (-1: dead), its LM and boosting
+  // rows there and whether the slot fills them; lane q of gch0[h]: the first
+  // chunk of group q + 64 h (at most one group per live slot)
+  int grp[SPL], lrow_g[SPL], brow_g[SPL], gch0[SPL];
+  bool lown[SPL], bown[SPL];
+#pragma unroll
+  for (int h = 0; h < SPL; ++h) {
+    grp[h] = 0;
+    lrow_g[h] = 0;
+    brow_g[h] = 0;
+    gch0[h] = 0;
+    lown[h] = bown[h] = h == 0 && j == 0;
+  }
+  int ngrp = 1;
 #pragma unroll
   for (int h = 0; h < SPL; ++h) {
     sc[h] = (h == 0 && j == 0) ? 0.0f : kNegInf;
@@ -398,8 +400,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // (bits 8..15)
   auto put_row = [&](int lp, int h) __attribute__((always_inline)) {
     uint32_t* rr = s_row + lp * kRowWords;
-    uint32_t zf = static_cast<uint32_t>(j + 64 * h) | (CACHE ? static_cast<uint32_t>(rowof) << 8 : 0u);
-    if constexpr (kGroups) zf |= (static_cast<uint32_t>(lrow_g) << 8) | (static_cast<uint32_t>(brow_g) << 16);
+    const uint32_t zf = static_cast<uint32_t>(j + 64 * h) | (CACHE ? static_cast<uint32_t>(rowof) << 8 : 0u) |
+                        (kGroups ? (static_cast<uint32_t>(lrow_g[h]) << 8) | (static_cast<uint32_t>(brow_g[h]) << 16) : 0u);
     *reinterpret_cast<uint4*>(rr) = make_uint4(__float_as_uint(sc[h]), static_cast<uint32_t>(last[h]),
                                                zf, static_cast<uint32_t>(btpot[h]));
 #pragma unroll
@@ -413,6 +415,149 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 #pragma unroll
   for (int h = 0; h < SPL; ++h) cid[h] = 0;
   int nch = 1;
+  // kGroups: the fill-group plan of the next frame from the new beam (nal:
+  // live slots, ac: staged arcs, lk: LM state keys).  LM states are taken in
+  // order of their lowest slot and, within a state, boosting lists in order
+  // of their lowest slot (beams without a list with the first); a group
+  // takes such (state, list) runs while its rows and staging area have room,
+  // and its beams get consecutive live positions, kcg to a chunk.  A group
+  // holds at most KCR - 1 lists: beams without a list read row KCR - 1,
+  // which the group's fill leaves empty.  Sets the live positions lpos, the
+  // group fields and chunk ids of the slots, nch, ngrp and gch0.
+  const auto plan_groups = [&](const bool (&nal)[SPL], const int32_t (&ac)[SPL], const uint32_t (&lk)[SPL],
+                               int (&lpos)[SPL]) __attribute__((always_inline)) {
+    uint64_t rem[SPL], hbm[SPL];
+    bool hasb[SPL];
+#pragma unroll
+    for (int h = 0; h < SPL; ++h) {
+      rem[h] = __ballot(nal[h]);
+      hasb[h] = HAS_BT && nal[h] && btc[h] != 0u;
+      hbm[h] = __ballot(hasb[h]);
+      grp[h] = -1;
+      lrow_g[h] = 0;
+      brow_g[h] = KCR - 1;
+      lown[h] = bown[h] = false;
+      cid[h] = -1;
+    }
+    const auto any = [&](const uint64_t (&m)[SPL]) __attribute__((always_inline)) {
+      bool r = false;
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) r = r || m[h] != 0ull;
+      return r;
+    };
+    // the register set holding the lowest slot of a non-empty mask
+    const auto low_set = [&](const uint64_t (&m)[SPL]) __attribute__((always_inline)) {
+      int hs = SPL - 1;
+#pragma unroll
+      for (int h = SPL - 1; h >= 0; --h) hs = m[h] != 0ull ? h : hs;
+      return hs;
+    };
+    int pos = 0, g = -1, chn = 0;
+    int g_rows = 0, g_arcs = 0, g_beams = 0, g_nbl = 0;
+#pragma unroll
+    for (int h = 0; h < SPL; ++h) gch0[h] = 0x7FFFFFFF;
+    while (any(rem)) {  // uniform: one LM state a pass
+      const int hs = low_set(rem);
+      uint32_t sk = 0u;
+      int a = 0;
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        if (h == hs) {
+          const int js = static_cast<int>(__builtin_ctzll(rem[h]));
+          sk = rdlane(lk[h], js);
+          a = rdlane(ac[h], js);
+        }
+      }
+      uint64_t smem[SPL];
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        smem[h] = __ballot(nal[h] && lk[h] == sk);
+        rem[h] &= ~smem[h];
+      }
+      int srow = -1;  // the state's LM row in the current group
+      while (any(smem)) {  // uniform: one boosting list a pass
+        const int hb = low_set(smem);
+        int jb = 0;
+        bool lb = false;
+        uint32_t b0 = 0u, c0 = 0u;
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          if (h == hb) {
+            jb = static_cast<int>(__builtin_ctzll(smem[h]));
+            lb = ((hbm[h] >> jb) & 1ull) != 0ull;
+            b0 = rdlane(btb[h], jb);
+            c0 = rdlane(btc[h], jb);
+          }
+        }
+        uint64_t sub[SPL];
+        bool samel[SPL];
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          samel[h] = hasb[h] && btb[h] == b0 && btc[h] == c0;
+          sub[h] = smem[h] & (lb ? __ballot(samel[h]) : ~hbm[h]);
+          smem[h] &= ~sub[h];
+        }
+        // the list's row, when the current group holds the list already
+        int brow = KCR - 1;
+        bool found = false;
+        if (lb && g >= 0) {
+#pragma unroll
+          for (int h = 0; h < SPL; ++h) {
+            const uint64_t fm = __ballot(samel[h] && grp[h] == g);
+            if (!found && fm != 0ull) {
+              found = true;
+              brow = rdlane(brow_g[h], static_cast<int>(__builtin_ctzll(fm)));
+            }
+          }
+        }
+        const bool need_lm = srow < 0;
+        const bool need_bl = lb && !found;
+        const bool fits = g >= 0 && (!need_lm || (g_rows < KSEG && g_arcs + a <= kLmStage)) &&
+                          (!need_bl || g_nbl < KCR - 1);
+        if (!fits) {
+          if (g >= 0) chn += (g_beams + kcg - 1) / kcg;
+          ++g;
+#pragma unroll
+          for (int h = 0; h < SPL; ++h)
+            if (h == (g >> 6) && lane == (g & 63)) gch0[h] = chn;
+          g_rows = 0;
+          g_arcs = 0;
+          g_beams = 0;
+          g_nbl = 0;
+          srow = -1;
+          found = false;
+          if (a > kLmStage) status |= 4u;  // a single chain above the staging limit (the builders prevent it)
+        }
+        const bool newrow = srow < 0;
+        if (newrow) {
+          srow = g_rows++;
+          g_arcs += a;
+        }
+        const bool newbl = lb && !found;
+        if (newbl) brow = g_nbl++;
+        int before = 0;  // members in the lower register sets
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          if ((sub[h] >> j) & 1ull) {
+            const int inq = before + __popcll(sub[h] & lmlt);
+            lpos[h] = pos + inq;
+            cid[h] = chn + (g_beams + inq) / kcg;
+            grp[h] = g;
+            lrow_g[h] = srow;
+            brow_g[h] = lb ? brow : KCR - 1;
+            lown[h] = newrow && h == hb && j == jb;
+            bown[h] = newbl && h == hb && j == jb;
+          }
+          before += __popcll(sub[h]);
+        }
+        g_beams += before;
+        pos += before;
+      }
+    }
+    if (g >= 0) chn += (g_beams + kcg - 1) / kcg;
+    nch = chn;
+    ngrp = g + 1;
+  };
   int rcur = 0;  // s_rec buffer holding the current beam
   // record helpers
   auto load_rec = [&](const uint32_t* src, uint32_t (&r)[RW]) {
@@ -570,30 +715,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       bool inch[SPL];
       int row[SPL];
       int kc = 0;
-      // kDedup: the chunk row whose LM row this beam reads (the lowest one
-      // with the same LM state), and whether it is that row's beam
-      int lrow = 0;
-      bool lfirst = true;
       if constexpr (SPL == 1) {
         inch[0] = alive[0] && (cid[0] == ch);
         const uint64_t chmask = __ballot(inch[0]);
         kc = __popcll(chmask);
         row[0] = __popcll(chmask & lmlt);
-        if constexpr (kDedup) {
-          lrow = row[0];
-          bool found = false;
-          for (uint64_t mm = chmask; mm != 0ull; mm &= mm - 1ull) {  // members in row order
-            const int jm = static_cast<int>(__builtin_ctzll(mm));
-            const bool same = !found && rdlane(lmsr, jm) == lmsr;
-            lrow = same ? rdlane(row[0], jm) : lrow;
-            found = found || same;
-          }
-          lfirst = lrow == row[0];
-          // the row table's slot field carries the LM row (wave 2 wrote the
-          // record in the update; the candidates read it after barrier A)
-          if (wave == 2 && inch[0])
-            s_row[(cs + row[0]) * kRowWords + 2] = static_cast<uint32_t>(j) | (static_cast<uint32_t>(lrow) << 8);
-        }
       } else {
 #pragma unroll
         for (int h = 0; h < SPL; ++h) {
@@ -606,26 +732,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 
       // ---- F. fill the key rows of this chunk (of its group) ----
       // kGroups: only a group's first chunk fills (uniform)
-      const bool gfill = !kGroups || (gi < ngrp && ch == rdlane(gch0, gi));
-      // the fill's beams: slots that fill an LM row / a boosting row, and the rows
-      const auto lm_sel = [&](int h) __attribute__((always_inline)) {
-        if constexpr (CACHE) return fillrep;
-        else if constexpr (kGroups) return alive[h] && grp == gi && lown;
-        else return inch[h] && lfirst;
-      };
-      const auto lm_rowof = [&](int h) __attribute__((always_inline)) {
-        if constexpr (CACHE) return rowof;
-        else if constexpr (kGroups) return lrow_g;
-        else return row[h];
-      };
-      const auto bt_sel = [&](int h) __attribute__((always_inline)) {
-        if constexpr (kGroups) return alive[h] && grp == gi && bown;
-        else return inch[h];
-      };
-      const auto bt_rowof = [&](int h) __attribute__((always_inline)) {
-        if constexpr (kGroups) return brow_g;
-        else return row[h];
-      };
+      bool gfill = !kGroups;
+      if constexpr (kGroups) {
+#pragma unroll
+        for (int h = 0; h < SPL; ++h)
+          if (h == (gi >> 6)) gfill = gi < ngrp && ch == rdlane(gch0[h], gi & 63);
+      }
       if (gfill) {  // uniform
         if (gen == kGenMax) {
           // rows were last read before the previous filter barrier
@@ -652,7 +764,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         for (int l = 0; l < NL; ++l) {
 #pragma unroll
           for (int h = 0; h < SPL; ++h) {
-            const uint32_t n = lm_sel(h) ? (lvc[h][l] & ~kExists) : 0u;
+            // the beams that fill an LM row (the row's first with fill groups)
+            const bool fsel = CACHE ? fillrep : kGroups ? (alive[h] && grp[h] == gi && lown[h]) : inch[h];
+            const uint32_t n = fsel ? (lvc[h][l] & ~kExists) : 0u;
             const uint64_t m = __ballot(n != 0u);
             const int nl = __popcll(m);
             if (nl > 0) {  // wave-uniform
@@ -664,7 +778,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               const uint32_t r_base =
                   static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(lvb[h][l])));
               const uint32_t r_rl =
-                  static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, lm_rowof(h) | (l << 8)));
+                  static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, (CACHE ? rowof : kGroups ? lrow_g[h] : row[h]) | (l << 8)));
               float r_f[NF];
 #pragma unroll
               for (int k = 0; k + 1 < NL; ++k) {
@@ -689,11 +803,11 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           // the explicit arcs (order >= 1) win the maximum
 #pragma unroll
           for (int h = 0; h < SPL; ++h) {
-            uint64_t fm = __ballot(lm_sel(h));
+            uint64_t fm = __ballot(kGroups ? (alive[h] && grp[h] == gi && lown[h]) : inch[h]);
             while (fm != 0ull) {  // uniform
               const int jr = static_cast<int>(__builtin_ctzll(fm));
               fm &= fm - 1ull;
-              const uint32_t rf = rdlane(static_cast<uint32_t>(lm_rowof(h)), jr);
+              const uint32_t rf = rdlane(static_cast<uint32_t>(kGroups ? lrow_g[h] : row[h]), jr);
               float bo[NLA];
 #pragma unroll
               for (int l = 0; l < NL; ++l) bo[l] = rdlane(lvbo[h][l], jr);
@@ -795,7 +909,9 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         uint32_t bg_cnt = 0u, bg_base = 0u, bg_row = 0u;
 #pragma unroll
         for (int h = 0; h < SPL; ++h) {
-          const uint32_t nb = bt_sel(h) ? btc[h] : 0u;
+          // the beams that fill a boosting row (the list's first with fill groups)
+          const bool bsel = kGroups ? (alive[h] && grp[h] == gi && bown[h]) : inch[h];
+          const uint32_t nb = bsel ? btc[h] : 0u;
           const uint64_t m = __ballot(nb != 0u);
           const int nl = __popcll(m);
           if (nl > 0) {  // wave-uniform
@@ -803,7 +919,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             const int addr = dst << 2;
             const uint32_t r_cnt = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(nb)));
             const uint32_t r_base = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, static_cast<int>(btb[h])));
-            const uint32_t r_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, bt_rowof(h)));
+            const uint32_t r_row = static_cast<uint32_t>(__builtin_amdgcn_ds_permute(addr, kGroups ? brow_g[h] : row[h]));
             if (lane >= S && lane < S + nl) {
               bg_cnt = r_cnt;
               bg_base = r_base;
@@ -866,8 +982,8 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         klast[i] = static_cast<int>(h0.y);
         // (uniform: fill groups keep the fields in scalar registers)
         const uint32_t hz = kGroups ? __builtin_amdgcn_readfirstlane(h0.z) : h0.z;
-        kslot[i] = static_cast<int>((CACHE || kDedup || kGroups) ? (hz & 0xFFu) : hz);
-        krow[i] = (CACHE || kDedup || kGroups) ? ((hz >> 8) & 0xFFu) : static_cast<uint32_t>(i);
+        kslot[i] = static_cast<int>((CACHE || kGroups) ? (hz & 0xFFu) : hz);
+        krow[i] = (CACHE || kGroups) ? ((hz >> 8) & 0xFFu) : static_cast<uint32_t>(i);
         kbrow[i] = kGroups ? ((hz >> 16) & 0xFFu) : static_cast<uint32_t>(i);
         kpot[i] = static_cast<int>(h0.w);
 #pragma unroll
@@ -894,7 +1010,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           const int c = tid + jj * kThreads;
           const uint32_t e = static_cast<uint32_t>(i * V) + rcc[jj];
           // LM entry: the row this beam reads (shared with its state's first beam)
-          const uint32_t el = (kDedup || kGroups) ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
+          const uint32_t el = kGroups ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
           const float x0 = ksc[i] + rD[jj];
           float x1 = x0 + beta;
           if (HAS_LM) {
@@ -973,10 +1089,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           if constexpr (CACHE) {
             av = __uint_as_float(static_cast<uint32_t>(lmrow[row * static_cast<uint32_t>(V) + c]));
           } else if constexpr (kFoldRows) {
-            const uint32_t el = (kDedup || kGroups) ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
+            const uint32_t el = kGroups ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
             av = __uint_as_float(static_cast<uint32_t>(lmrow[el]));
           } else {
-            const uint32_t el = (kDedup || kGroups) ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
+            const uint32_t el = kGroups ? ((rr[2] >> 8) & 0xFFu) * static_cast<uint32_t>(V) + c : e;
             const uint64_t ent = lmrow[el];
             if (static_cast<uint32_t>(ent >> 32) >= genhi) {
               av = __uint_as_float(static_cast<uint32_t>(ent));
@@ -1003,7 +1119,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
 #pragma unroll 1
         for (int q = 0; q < kc; ++q) {
           const uint32_t z = s_row[(cs + q) * kRowWords + 2];
-          if (((CACHE || kDedup || kGroups) ? (z & 0xFFu) : z) == slot) {
+          if (((CACHE || kGroups) ? (z & 0xFFu) : z) == slot) {
             i = static_cast<uint32_t>(q);
             row = (z >> 8) & 0xFFu;
           }
@@ -1021,7 +1137,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           if constexpr (CACHE) {
             lraw = static_cast<uint32_t>(lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]] >> 32) & kTargetMask;
           } else {
-            const uint32_t el = (kDedup || kGroups) ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
+            const uint32_t el = kGroups ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
             const uint32_t hi = static_cast<uint32_t>(lmrow[el] >> 32);
             lraw = (kFoldRows || hi >= genhi) ? hi : rcc[jj];
           }
@@ -1442,7 +1558,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   wflat = flat;
                   wi = static_cast<uint32_t>(i);
                   wjj = static_cast<uint32_t>(jj);
-                  if constexpr (CACHE || kDedup || kGroups) wrow = krow[i];
+                  if constexpr (CACHE || kGroups) wrow = krow[i];
                   if constexpr (kGroups) wbrow = kbrow[i];
                 }
               }
@@ -1490,7 +1606,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
                   if constexpr (CACHE) {
                     lmt = static_cast<uint32_t>(lmrow[wrow * static_cast<uint32_t>(V) + c] >> 32) & kTargetMask;
                   } else {
-                    const uint32_t el = (kDedup || kGroups) ? wrow * static_cast<uint32_t>(V) + c : e;
+                    const uint32_t el = kGroups ? wrow * static_cast<uint32_t>(V) + c : e;
                     const uint32_t hi = static_cast<uint32_t>(lmrow[el] >> 32);
                     lmt = (kFoldRows || hi >= genhi) ? lm_target(hi) : c;
                   }
@@ -1626,7 +1742,6 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       last[0] = nlast;
       len[0] = nlen;
       alive[0] = nalive;
-      if constexpr (kDedup) lmsr = nalive ? rec[kRLms] : 0xFFFFFFFFu;
       int32_t acnt = 0;
 #pragma unroll
       for (int l = 0; l < NL; ++l) {
@@ -1725,119 +1840,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         }
       }
       if constexpr (kGroups) {
-        // Fill groups of the next frame.  LM states are taken in order of
-        // their lowest slot and, within a state, boosting lists in order of
-        // their lowest slot (beams without a list first); a group takes such
-        // (state, list) runs while its rows and staging area have room, and
-        // its beams get consecutive live positions, kcg to a chunk.  A group
-        // holds at most KCR - 1 lists: beams without a list read row KCR - 1,
-        // which the group's fill leaves empty.  Lane q of gch0, gmem and gbl:
-        // the first chunk, the member slots and the list set of group q.
-        const auto rd64 = [&](uint64_t v, int l) __attribute__((always_inline)) {
-          return (static_cast<uint64_t>(rdlane(static_cast<uint32_t>(v >> 32), l)) << 32) |
-                 rdlane(static_cast<uint32_t>(v), l);
-        };
-        const auto bperm64 = [&](uint64_t v, int l) __attribute__((always_inline)) {
-          const int a = l << 2;
-          return (static_cast<uint64_t>(static_cast<uint32_t>(
-                      __builtin_amdgcn_ds_bpermute(a, static_cast<int>(static_cast<uint32_t>(v >> 32)))))
-                  << 32) |
-                 static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(a, static_cast<int>(static_cast<uint32_t>(v))));
-        };
-        const uint32_t lkey = (HAS_LM && NL > 0) ? rec[kRLms] : 0u;  // a unigram LM fills no row
-        // distinct boosting lists (begin, count) of the live beams, numbered
-        // in order of their lowest slot; lane k of bmk: the slots holding list k
-        const bool hasb = HAS_BT && nalive && btc[0] != 0u;
-        const uint64_t hbm = __ballot(hasb);
-        int bidx = 0;
-        uint64_t bmk = 0ull;
-        if constexpr (HAS_BT) {
-          uint64_t brem = hbm;
-          int nbl = 0;
-          while (brem != 0ull) {  // uniform
-            const int jm = static_cast<int>(__builtin_ctzll(brem));
-            const uint32_t b0 = rdlane(btb[0], jm), c0 = rdlane(btc[0], jm);
-            const uint64_t m = __ballot(hasb && btb[0] == b0 && btc[0] == c0);
-            brem &= ~m;
-            if (lane == nbl) bmk = m;
-            if ((m >> j) & 1ull) bidx = nbl;
-            ++nbl;
-          }
-        }
-        uint64_t rem = amask;
-        uint64_t gmem = 0ull, gbl = 0ull;
-        int pos = 0, g = -1, chn = 0;
-        int g_rows = 0, g_arcs = 0, g_beams = 0;
-        uint64_t g_bl = 0ull;
-        gch0 = 0x7FFFFFFF;
-        grp = -1;
-        lown = false;
-        cid[0] = -1;
-        while (rem != 0ull) {  // uniform: one LM state a pass
-          const int js = static_cast<int>(__builtin_ctzll(rem));
-          const uint32_t sk = rdlane(lkey, js);
-          uint64_t smem = __ballot(nalive && lkey == sk);
-          rem &= ~smem;
-          const int a = rdlane(acnt, js);
-          int srow = -1;  // the state's LM row in the current group
-          while (smem != 0ull) {  // uniform: one boosting list a pass
-            const int jb = static_cast<int>(__builtin_ctzll(smem));
-            int kb = -1;
-            uint64_t sub = smem & ~hbm;
-            if (HAS_BT && ((hbm >> jb) & 1ull)) {
-              kb = rdlane(bidx, jb);
-              sub = smem & rd64(bmk, kb);
-            }
-            smem &= ~sub;
-            const bool need_lm = srow < 0;
-            const bool need_bl = kb >= 0 && !((g_bl >> kb) & 1ull);
-            const bool fits = g >= 0 && (!need_lm || (g_rows < KSEG && g_arcs + a <= kLmStage)) &&
-                              (!need_bl || __popcll(g_bl) < KCR - 1);
-            if (!fits) {
-              if (g >= 0) chn += (g_beams + kcg - 1) / kcg;
-              ++g;
-              if (lane == g) gch0 = chn;
-              g_rows = 0;
-              g_arcs = 0;
-              g_beams = 0;
-              g_bl = 0ull;
-              srow = -1;
-              if (a > kLmStage) status |= 4u;  // a single chain above the staging limit (the builders prevent it)
-            }
-            const bool newrow = srow < 0;
-            if (newrow) {
-              srow = g_rows++;
-              g_arcs += a;
-            }
-            if (kb >= 0) g_bl |= 1ull << kb;
-            if ((sub >> j) & 1ull) {
-              const int inq = __popcll(sub & lmlt);
-              lp = pos + inq;
-              cid[0] = chn + (g_beams + inq) / kcg;
-              grp = g;
-              lrow_g = srow;
-              lown = newrow && j == jb;
-            }
-            if (lane == g) {
-              gmem |= sub;
-              gbl = g_bl;
-            }
-            const int cnt = __popcll(sub);
-            g_beams += cnt;
-            pos += cnt;
-          }
-        }
-        if (g >= 0) chn += (g_beams + kcg - 1) / kcg;
-        nch = chn;
-        ngrp = g + 1;
-        if constexpr (HAS_BT) {
-          // list k's row in group q: its rank among the group's lists; the
-          // group's lowest slot holding it fills the row
-          const int gq = max(grp, 0);
-          const uint64_t mg = bperm64(gmem, gq), bg = bperm64(gbl, gq), mk = bperm64(bmk, bidx);
-          brow_g = hasb ? __popcll(bg & ((1ull << bidx) - 1ull)) : KCR - 1;
-          bown = hasb && static_cast<int>(__builtin_ctzll(mk & mg)) == j;
-        }
+        const bool nal[1] = {nalive};
+        const int32_t ac[1] = {acnt};
+        const uint32_t lk[1] = {(HAS_LM && NL > 0 && nalive) ? rec[kRLms] : 0u};  // a unigram LM fills no row
+        int lpa[1] = {lp};
+        plan_groups(nal, ac, lk, lpa);
+        lp = lpa[0];
       }
       if (wave == 2 && nalive) put_row(lp, 0);
       // chunk plan: live slots in slot order, at most kcmax beams and
@@ -2043,13 +2051,21 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         const uint64_t amask = __ballot(nalive[h]);
         lp[h] = na + __popcll(amask & lmlt);
         na += __popcll(amask);
-        if (wave == 2 && nalive[h]) put_row(lp[h], h);
+        if (!kGroups && wave == 2 && nalive[h]) put_row(lp[h], h);
         ia[h] = tota + wave_incl_scan(acnt[h], lane);
         tota = rdlane(ia[h], 63);
       }
-      // chunk plan: live slots in slot order, at most kcmax beams and
-      // kLmStage staged arcs per chunk
-      if (na <= kcmax && tota <= kLmStage) {
+      if constexpr (kGroups) {
+        uint32_t lk[SPL];
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) lk[h] = (HAS_LM && NL > 0 && nalive[h]) ? rec[h][kRLms] : 0u;
+        plan_groups(nalive, acnt, lk, lp);
+#pragma unroll
+        for (int h = 0; h < SPL; ++h)
+          if (wave == 2 && nalive[h]) put_row(lp[h], h);
+      } else if (na <= kcmax && tota <= kLmStage) {
+        // chunk plan: live slots in slot order, at most kcmax beams and
+        // kLmStage staged arcs per chunk
         nch = na > 0 ? 1 : 0;
 #pragma unroll
         for (int h = 0; h < SPL; ++h) cid[h] = 0;

@@ -1,17 +1,19 @@
-"""GPU parity of shared LM rows: with a 5-gram or higher-order LM, no row
-cache and one beam slot per lane, beams of one chunk that sit in the same LM
-state read one LM row (filled once) instead of one row each.  Sharing
-changes which rows are filled, never a score, so the results must equal the
-CPU oracle's (tokens bit-exact, scores within 1e-4).
+"""GPU parity of fill groups: with beams over one chunk (K above 16 / labels
+per lane) and no row cache, beams in the same LM state read one LM row and
+beams with the same boosting list one boosting row, filled once for a group
+of consecutive chunks.  Sharing changes which rows are filled, never a score,
+so the results must equal the CPU oracle's (tokens bit-exact, scores within
+1e-4).
 
 * 5- and 6-gram LMs of a few thousand n-grams (most hypotheses back off to
-  short, shared states) with K = 9..64, vocabularies of 300, 1024 and 1500
-  tokens (one, two and four labels per lane), with and without boosting,
-  theta = inf and 12, 1-best and N-best;
+  short, shared states) with K = 9..128 (one and two beam slots per lane),
+  vocabularies of 300, 400, 1024 and 1500 tokens (one, two and four labels
+  per lane), with and without boosting, theta = inf and 12, 1-best and
+  N-best;
 * log-sum-exp recombination and repeat scoring on the same path;
 * a witness that the final beams do share LM states (the longest suffix of
-  <s> + tokens that is an n-gram of the model), so that the shared-row path
-  is the one these cases run.
+  <s> + tokens that is an n-gram of the model), so that shared rows are what
+  these cases run.
 """
 import math
 
@@ -67,7 +69,8 @@ def _lm_state(entries, order, bos, toks):
 
 @pytest.mark.parametrize("order,V,K,boost", [
     (5, 1024, 16, False), (5, 1024, 64, True), (6, 1024, 40, True), (6, 1024, 64, False),
-    (6, 1024, 9, True), (6, 300, 33, True), (5, 1500, 64, False), (5, 1500, 24, True)])
+    (6, 1024, 9, True), (6, 300, 33, True), (5, 1500, 64, False), (5, 1500, 24, True),
+    (6, 1024, 100, True), (5, 1024, 128, False), (6, 400, 77, True)])
 def test_shared_rows(order, V, K, boost):
     w = _workload(order, V, K, boost, 31000 + 97 * order + K)
     lm, bt, olm, obt = handles(w)
@@ -90,7 +93,7 @@ def test_shared_rows_random_logits(seed):
     rng = np.random.default_rng(32000 + seed)
     V = int(rng.choice([200, 700, 1024]))
     order = int(rng.integers(5, 8 if V <= 500 else 7))  # LM ids need (V+2)^order < 2^62
-    K = int(rng.integers(9, 65))
+    K = int(rng.integers(9, 129))
     w = _workload(order, V, K, bool(rng.random() < 0.5), 32100 + seed)
     lm, bt, olm, obt = handles(w)
     B, T = 2, int(rng.integers(20, 70))
