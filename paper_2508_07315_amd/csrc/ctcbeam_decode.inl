@@ -165,8 +165,10 @@ __device__ __forceinline__ bool dup_by_sort(uint64_t key, int lane, uint32_t& lo
 // Per-phase clocks (profiling builds, -DCTCBEAM_PHASE_CLOCKS; the macro is in
 // ctcbeam_internal.h): each wave adds the s_memtime cycles of every phase of
 // every frame (fill, barrier A, candidates, barrier B, filter, barrier C,
-// rank, barrier D, update; then the frame and chunk counts) and writes them
-// after the [B, 8] statistics as [B, kWaves, kPhaseWords] int64.
+// rank, barrier D, the update's remainder; then the frame and chunk counts;
+// then, one slot per lane, the update's prune + recombination, new state and
+// chunk plan) and writes them after the [B, 8] statistics as
+// [B, kWaves, kPhaseWords] int64.
 
 // SPL = beam slots per lane: slot j lives in lane j % 64, register set
 // j / 64 (SPL = 2 serves beams of 65..128).  SKIP: ranks of chunks before
@@ -291,7 +293,6 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   const int b = blockIdx.x;
   const int V = p.V, W = V + 1, K = p.K, T = p.T;
   const int kcmax = min(K, KSEG);
-  const int kcg = min(K, KCR);  // beams per chunk with fill groups
   const float alpha = p.alpha, beta = p.beta, boost_w = p.boost_w;
   const uint64_t lmlt = lanemask_lt();
   // repeat-scoring variant: a repeated token gets its LM / boosting terms again
@@ -417,28 +418,17 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   int nch = 1;
   // kGroups: the fill-group plan of the next frame from the new beam (nal:
   // live slots, ac: staged arcs, lk: LM state keys).  LM states are taken in
-  // order of their lowest slot and, within a state, boosting lists in order
-  // of their lowest slot (beams without a list with the first); a group
-  // takes such (state, list) runs while its rows and staging area have room,
-  // and its beams get consecutive live positions, kcg to a chunk.  A group
-  // holds at most KCR - 1 lists: beams without a list read row KCR - 1,
-  // which the group's fill leaves empty.  Sets the live positions lpos, the
-  // group fields and chunk ids of the slots, nch, ngrp and gch0.
+  // order of their lowest slot; a group takes whole states while its LM rows,
+  // staging area and boosting lists have room, and its beams get consecutive
+  // live positions, KCR to a chunk (a state whose own lists exceed a group is
+  // split by list).  A boosting list is named by its leader, its lowest slot;
+  // in a group it gets the rank of its leader among the group's lists as its
+  // row, and its lowest member in the group fills the row.  A group holds at
+  // most KCR - 1 lists: beams without a list read row KCR - 1, which the
+  // group's fill leaves empty.  Sets the live positions lpos, the group
+  // fields and chunk ids of the slots, nch, ngrp and gch0.
   const auto plan_groups = [&](const bool (&nal)[SPL], const int32_t (&ac)[SPL], const uint32_t (&lk)[SPL],
                                int (&lpos)[SPL]) __attribute__((always_inline)) {
-    uint64_t rem[SPL], hbm[SPL];
-    bool hasb[SPL];
-#pragma unroll
-    for (int h = 0; h < SPL; ++h) {
-      rem[h] = __ballot(nal[h]);
-      hasb[h] = HAS_BT && nal[h] && btc[h] != 0u;
-      hbm[h] = __ballot(hasb[h]);
-      grp[h] = -1;
-      lrow_g[h] = 0;
-      brow_g[h] = KCR - 1;
-      lown[h] = bown[h] = false;
-      cid[h] = -1;
-    }
     const auto any = [&](const uint64_t (&m)[SPL]) __attribute__((always_inline)) {
       bool r = false;
 #pragma unroll
@@ -452,109 +442,212 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       for (int h = SPL - 1; h >= 0; --h) hs = m[h] != 0ull ? h : hs;
       return hs;
     };
-    int pos = 0, g = -1, chn = 0;
-    int g_rows = 0, g_arcs = 0, g_beams = 0, g_nbl = 0;
+    const auto rd64 = [&](uint64_t v, int l) __attribute__((always_inline)) {
+      return (static_cast<uint64_t>(rdlane(static_cast<uint32_t>(v >> 32), l)) << 32) |
+             rdlane(static_cast<uint32_t>(v), l);
+    };
+    uint64_t rem[SPL], hbm[SPL];
+    bool hasb[SPL], lead[SPL];
+    int bl[SPL];             // leader of the slot's boosting list
+    uint64_t lmk[SPL][SPL];  // the slots holding the slot's list, by register set
 #pragma unroll
-    for (int h = 0; h < SPL; ++h) gch0[h] = 0x7FFFFFFF;
+    for (int h = 0; h < SPL; ++h) {
+      rem[h] = __ballot(nal[h]);
+      hasb[h] = HAS_BT && nal[h] && btc[h] != 0u;
+      hbm[h] = __ballot(hasb[h]);
+      lead[h] = false;
+      bl[h] = 0;
+#pragma unroll
+      for (int hh = 0; hh < SPL; ++hh) lmk[h][hh] = 0ull;
+      grp[h] = -1;
+      lrow_g[h] = 0;
+      brow_g[h] = KCR - 1;
+      lown[h] = bown[h] = false;
+      cid[h] = -1;
+      gch0[h] = 0x7FFFFFFF;
+    }
+    if constexpr (HAS_BT) {
+      // the distinct lists (begin, count): one a pass
+      uint64_t brem[SPL];
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) brem[h] = hbm[h];
+      while (any(brem)) {  // uniform
+        const int hl = low_set(brem);
+        int jl = 0;
+        uint32_t b0 = 0u, c0 = 0u;
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          if (h == hl) {
+            jl = static_cast<int>(__builtin_ctzll(brem[h]));
+            b0 = rdlane(btb[h], jl);
+            c0 = rdlane(btc[h], jl);
+          }
+        }
+        uint64_t m[SPL];
+#pragma unroll
+        for (int hh = 0; hh < SPL; ++hh) {
+          m[hh] = __ballot(hasb[hh] && btb[hh] == b0 && btc[hh] == c0);
+          brem[hh] &= ~m[hh];
+        }
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          if ((m[h] >> j) & 1ull) {
+            bl[h] = jl + 64 * hl;
+#pragma unroll
+            for (int hh = 0; hh < SPL; ++hh) lmk[h][hh] = m[hh];
+          }
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) lead[h] = hasb[h] && bl[h] == j + 64 * h;
+    }
+    int pos = 0, g = -1, chn = 0;
+    int g_rows = 0, g_arcs = 0, g_beams = 0;
+    uint64_t g_bl[SPL], g_mem[SPL];  // the open group's lists (by leader) and members
+#pragma unroll
+    for (int h = 0; h < SPL; ++h) g_bl[h] = g_mem[h] = 0ull;
+    // the open group's chunks, and its members' boosting rows and fillers
+    const auto close_group = [&]() __attribute__((always_inline)) {
+      if (g < 0) return;
+      chn += (g_beams + KCR - 1) / KCR;
+      if constexpr (HAS_BT) {
+#pragma unroll
+        for (int h = 0; h < SPL; ++h) {
+          if (grp[h] == g && hasb[h]) {
+            const int L = bl[h];
+            int r = 0;
+            bool first = true;
+#pragma unroll
+            for (int hh = 0; hh < SPL; ++hh) {
+              const uint64_t lead_below =
+                  hh < (L >> 6) ? ~0ull : (hh == (L >> 6) ? ((1ull << (L & 63)) - 1ull) : 0ull);
+              r += __popcll(g_bl[hh] & lead_below);
+              const uint64_t slot_below = hh < h ? ~0ull : (hh == h ? lmlt : 0ull);
+              first = first && (lmk[h][hh] & g_mem[hh] & slot_below) == 0ull;
+            }
+            brow_g[h] = r;
+            bown[h] = first;
+          }
+        }
+      }
+    };
+    const auto open_group = [&](int a) __attribute__((always_inline)) {
+      close_group();
+      ++g;
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        if (h == (g >> 6) && lane == (g & 63)) gch0[h] = chn;
+        g_bl[h] = g_mem[h] = 0ull;
+      }
+      g_rows = 0;
+      g_arcs = 0;
+      g_beams = 0;
+      if (a > kLmStage) status |= 4u;  // a single chain above the staging limit (the builders prevent it)
+    };
+    // the beams sub join the open group with LM row srow (filled by beam
+    // (hs, js) when the row is new) and bring the lists nl
+    const auto place = [&](const uint64_t (&sub)[SPL], const uint64_t (&nl)[SPL], int srow, bool newrow, int hs,
+                           int js) __attribute__((always_inline)) {
+      int before = 0;  // members in the lower register sets
+#pragma unroll
+      for (int h = 0; h < SPL; ++h) {
+        if ((sub[h] >> j) & 1ull) {
+          const int inq = before + __popcll(sub[h] & lmlt);
+          lpos[h] = pos + inq;
+          cid[h] = chn + (g_beams + inq) / KCR;
+          grp[h] = g;
+          lrow_g[h] = srow;
+          lown[h] = newrow && h == hs && j == js;
+        }
+        before += __popcll(sub[h]);
+        g_mem[h] |= sub[h];
+        g_bl[h] |= nl[h];
+      }
+      g_beams += before;
+      pos += before;
+    };
     while (any(rem)) {  // uniform: one LM state a pass
       const int hs = low_set(rem);
+      int js = 0, a = 0;
       uint32_t sk = 0u;
-      int a = 0;
 #pragma unroll
       for (int h = 0; h < SPL; ++h) {
         if (h == hs) {
-          const int js = static_cast<int>(__builtin_ctzll(rem[h]));
+          js = static_cast<int>(__builtin_ctzll(rem[h]));
           sk = rdlane(lk[h], js);
           a = rdlane(ac[h], js);
         }
       }
-      uint64_t smem[SPL];
+      uint64_t smem[SPL], sl[SPL];
+      int nsl = 0, nu = 0;
 #pragma unroll
       for (int h = 0; h < SPL; ++h) {
         smem[h] = __ballot(nal[h] && lk[h] == sk);
         rem[h] &= ~smem[h];
       }
-      int srow = -1;  // the state's LM row in the current group
-      while (any(smem)) {  // uniform: one boosting list a pass
-        const int hb = low_set(smem);
-        int jb = 0;
-        bool lb = false;
-        uint32_t b0 = 0u, c0 = 0u;
+      // the state's lists, by leader
 #pragma unroll
-        for (int h = 0; h < SPL; ++h) {
-          if (h == hb) {
-            jb = static_cast<int>(__builtin_ctzll(smem[h]));
-            lb = ((hbm[h] >> jb) & 1ull) != 0ull;
-            b0 = rdlane(btb[h], jb);
-            c0 = rdlane(btc[h], jb);
-          }
-        }
-        uint64_t sub[SPL];
-        bool samel[SPL];
+      for (int h = 0; h < SPL; ++h) {
+        bool pres = false;
 #pragma unroll
-        for (int h = 0; h < SPL; ++h) {
-          samel[h] = hasb[h] && btb[h] == b0 && btc[h] == c0;
-          sub[h] = smem[h] & (lb ? __ballot(samel[h]) : ~hbm[h]);
-          smem[h] &= ~sub[h];
-        }
-        // the list's row, when the current group holds the list already
-        int brow = KCR - 1;
-        bool found = false;
-        if (lb && g >= 0) {
+        for (int hh = 0; hh < SPL; ++hh) pres = pres || (lmk[h][hh] & smem[hh]) != 0ull;
+        sl[h] = __ballot(lead[h] && pres);
+        nsl += __popcll(sl[h]);
+        nu += __popcll(sl[h] | g_bl[h]);
+      }
+      if (nsl <= KCR - 1) {  // uniform: the whole state joins one group
+        if (!(g >= 0 && g_rows < KSEG && g_arcs + a <= kLmStage && nu <= KCR - 1)) open_group(a);
+        const int srow = g_rows++;
+        g_arcs += a;
+        place(smem, sl, srow, true, hs, js);
+      } else {
+        // the state's lists exceed a group: one list a pass (beams without a
+        // list with the lowest slot's pass)
+        int srow = -1;
+        while (any(smem)) {  // uniform
+          const int hb = low_set(smem);
+          int jb = 0, L = 0;
+          bool lb = false;
 #pragma unroll
           for (int h = 0; h < SPL; ++h) {
-            const uint64_t fm = __ballot(samel[h] && grp[h] == g);
-            if (!found && fm != 0ull) {
-              found = true;
-              brow = rdlane(brow_g[h], static_cast<int>(__builtin_ctzll(fm)));
+            if (h == hb) {
+              jb = static_cast<int>(__builtin_ctzll(smem[h]));
+              lb = ((hbm[h] >> jb) & 1ull) != 0ull;
+              L = rdlane(bl[h], jb);
             }
           }
-        }
-        const bool need_lm = srow < 0;
-        const bool need_bl = lb && !found;
-        const bool fits = g >= 0 && (!need_lm || (g_rows < KSEG && g_arcs + a <= kLmStage)) &&
-                          (!need_bl || g_nbl < KCR - 1);
-        if (!fits) {
-          if (g >= 0) chn += (g_beams + kcg - 1) / kcg;
-          ++g;
+          uint64_t sub[SPL], nl[SPL];
+          bool newl = false;
+          int nb = 0;
 #pragma unroll
-          for (int h = 0; h < SPL; ++h)
-            if (h == (g >> 6) && lane == (g & 63)) gch0[h] = chn;
-          g_rows = 0;
-          g_arcs = 0;
-          g_beams = 0;
-          g_nbl = 0;
-          srow = -1;
-          found = false;
-          if (a > kLmStage) status |= 4u;  // a single chain above the staging limit (the builders prevent it)
-        }
-        const bool newrow = srow < 0;
-        if (newrow) {
-          srow = g_rows++;
-          g_arcs += a;
-        }
-        const bool newbl = lb && !found;
-        if (newbl) brow = g_nbl++;
-        int before = 0;  // members in the lower register sets
+          for (int hh = 0; hh < SPL; ++hh) {
+            uint64_t mk = 0ull;
 #pragma unroll
-        for (int h = 0; h < SPL; ++h) {
-          if ((sub[h] >> j) & 1ull) {
-            const int inq = before + __popcll(sub[h] & lmlt);
-            lpos[h] = pos + inq;
-            cid[h] = chn + (g_beams + inq) / kcg;
-            grp[h] = g;
-            lrow_g[h] = srow;
-            brow_g[h] = lb ? brow : KCR - 1;
-            lown[h] = newrow && h == hb && j == jb;
-            bown[h] = newbl && h == hb && j == jb;
+            for (int h = 0; h < SPL; ++h)
+              if (h == hb) mk = rd64(lmk[h][hh], jb);
+            sub[hh] = smem[hh] & (lb ? mk : ~hbm[hh]);
+            nl[hh] = (lb && hh == (L >> 6)) ? (1ull << (L & 63)) : 0ull;
+            newl = newl || (nl[hh] & ~g_bl[hh]) != 0ull;
+            nb += __popcll(g_bl[hh]);
           }
-          before += __popcll(sub[h]);
+          const bool fits = g >= 0 && (srow >= 0 || (g_rows < KSEG && g_arcs + a <= kLmStage)) &&
+                            (!newl || nb < KCR - 1);
+          if (!fits) {
+            open_group(a);
+            srow = -1;
+          }
+          const bool newrow = srow < 0;
+          if (newrow) {
+            srow = g_rows++;
+            g_arcs += a;
+          }
+          place(sub, nl, srow, newrow, hb, jb);
+#pragma unroll
+          for (int hh = 0; hh < SPL; ++hh) smem[hh] &= ~sub[hh];
         }
-        g_beams += before;
-        pos += before;
       }
     }
-    if (g >= 0) chn += (g_beams + kcg - 1) / kcg;
+    close_group();
     nch = chn;
     ngrp = g + 1;
   };
@@ -684,7 +777,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   int mpar = 0;  // reserved region holding the pool's reserved entries
   __syncthreads();
 #ifdef CTCBEAM_PHASE_CLOCKS
-  uint64_t ph_acc[kPhaseWords] = {};
+  uint64_t ph_acc = 0ull;
   uint64_t ph_t0 = __builtin_amdgcn_s_memtime();
 #endif
 
@@ -1363,9 +1456,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       if (SKIP && !last_chunk && !s_overflow && npool <= kCap / 2) {  // uniform
         carry = npool;
         cs += kc;
-#ifdef CTCBEAM_PHASE_CLOCKS
-        ph_acc[10] += 1;  // chunks
-#endif
+        CTCBEAM_PHASE_COUNT(10);  // chunks
         continue;
       }
       {
@@ -1660,9 +1751,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       CTCBEAM_PHASE_MARK(6);
       __syncthreads();  // D: best K of the chunk in region Q
       CTCBEAM_PHASE_MARK(7);
-#ifdef CTCBEAM_PHASE_CLOCKS
-      ph_acc[10] += 1;  // chunks
-#endif
+      CTCBEAM_PHASE_COUNT(10);  // chunks
       mpar ^= 1;
       carry = 0;
       if (ch + 1 < nch && nfin >= K) tau_run = fmaxf(tau_run, __uint_as_float(s_res[mpar][K - 1].x));
@@ -1732,6 +1821,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         }
       }
       if (dup) x = kNegInf;
+      CTCBEAM_PHASE_MARK(11);
       const bool nalive = alive0 && !dup;
       // back-pointers and beam records from waves 1 and 2: wave 0 carries the
       // frame's longest chain, and a store would hold its next load wait
@@ -1782,6 +1872,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         if (emit_fin) atomicAdd(&s_st[5], 1ull);
       }
       rcur ^= 1;
+      CTCBEAM_PHASE_MARK(12);
       // live positions and beam records for the next frame
       const uint64_t amask = __ballot(nalive);
       const int na = __popcll(amask);
@@ -1847,6 +1938,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         plan_groups(nal, ac, lk, lpa);
         lp = lpa[0];
       }
+      CTCBEAM_PHASE_MARK(13);
       if (wave == 2 && nalive) put_row(lp, 0);
       // chunk plan: live slots in slot order, at most kcmax beams and
       // kLmStage staged arcs per chunk (cached rows stage nothing)
@@ -2103,15 +2195,12 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     }
     }
     CTCBEAM_PHASE_MARK(8);
-#ifdef CTCBEAM_PHASE_CLOCKS
-    ph_acc[9] += 1;  // frames
-#endif
+    CTCBEAM_PHASE_COUNT(9);  // frames
   }
 #ifdef CTCBEAM_PHASE_CLOCKS
-  if (p.stats && lane == 0) {
+  if (p.stats && lane < kPhaseWords) {
     int64_t* pw = p.stats + static_cast<size_t>(p.B) * 8 + (static_cast<size_t>(b) * kWaves + wave) * kPhaseWords;
-#pragma unroll
-    for (int q = 0; q < kPhaseWords; ++q) pw[q] = static_cast<int64_t>(ph_acc[q]);
+    pw[lane] = static_cast<int64_t>(ph_acc);
   }
 #endif
 

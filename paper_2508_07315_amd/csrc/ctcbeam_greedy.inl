@@ -170,7 +170,7 @@ __global__ void __launch_bounds__(64 * NW) greedy_kernel(KernelParams p) {
   // barrier, the decision, chain headers + fold, continuations, row loads;
   // then frames and refills
 #ifdef CTCBEAM_PHASE_CLOCKS
-  uint64_t ph_acc[kPhaseWords] = {};
+  uint64_t ph_acc = 0ull;
   uint64_t ph_t0 = __builtin_amdgcn_s_memtime();
 #endif
 
@@ -187,9 +187,7 @@ __global__ void __launch_bounds__(64 * NW) greedy_kernel(KernelParams p) {
     }
     if (HAS_BT) nd = p.bt_nodes[btn];
     ++st_refill;
-#ifdef CTCBEAM_PHASE_CLOCKS
-    ph_acc[10] += 1;
-#endif
+    CTCBEAM_PHASE_COUNT(10);
     if (HAS_LM) {
       // unigram + backoff fold of every label (innermost context first)
 #pragma unroll
@@ -403,9 +401,7 @@ __global__ void __launch_bounds__(64 * NW) greedy_kernel(KernelParams p) {
       cw = V;
       xw = xblank;
     }
-#ifdef CTCBEAM_PHASE_CLOCKS
-    ph_acc[9] += 1;
-#endif
+    CTCBEAM_PHASE_COUNT(9);
     if (xw == kNegInf) {
       dead = true;
       return false;
@@ -548,10 +544,9 @@ __global__ void __launch_bounds__(64 * NW) greedy_kernel(KernelParams p) {
     for (int tt = nout + lane; tt < T; tt += 64) ot[tt] = -1;
   }
 #ifdef CTCBEAM_PHASE_CLOCKS
-  if (p.stats && lane == 0) {
+  if (p.stats && lane < kPhaseWords) {
     int64_t* pw = p.stats + static_cast<size_t>(p.B) * 8 + (static_cast<size_t>(b) * 8 + wave) * kPhaseWords;
-#pragma unroll
-    for (int q = 0; q < kPhaseWords; ++q) pw[q] = static_cast<int64_t>(ph_acc[q]);
+    pw[lane] = static_cast<int64_t>(ph_acc);
   }
 #endif
   if (tid == 0) {

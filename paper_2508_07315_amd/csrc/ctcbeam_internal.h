@@ -32,20 +32,29 @@ constexpr uint32_t kWsMagic = 0x42435443u;  // "CTCB"
 // LM state record, one per chain level l (context of length l+1):
 //   {arc_begin, arc_count | kExists, backoff bits}
 // Per-phase clocks of the kernels in profiling builds (-DCTCBEAM_PHASE_CLOCKS):
-// a kernel declares uint64_t ph_acc[kPhaseWords] and ph_t0, and each
-// CTCBEAM_PHASE_MARK(k) adds the s_memtime cycles since the previous mark to
-// word k.  Product builds compile none of it.
+// a kernel declares uint64_t ph_acc (lane k of each wave holds word k) and
+// ph_t0; each CTCBEAM_PHASE_MARK(k) adds the s_memtime cycles since the
+// previous mark to word k, CTCBEAM_PHASE_COUNT(k) adds one.  One register
+// pair per wave keeps the profiling build's register use close to the
+// product's.  Product builds compile none of it.
 constexpr int kPhaseWords = 16;
 #ifdef CTCBEAM_PHASE_CLOCKS
-#define CTCBEAM_PHASE_MARK(k)                          \
-  do {                                                 \
-    const uint64_t now_ = __builtin_amdgcn_s_memtime(); \
-    ph_acc[k] += now_ - ph_t0;                         \
-    ph_t0 = now_;                                      \
+#define CTCBEAM_PHASE_MARK(k)                                          \
+  do {                                                                 \
+    const uint64_t now_ = __builtin_amdgcn_s_memtime();                \
+    ph_acc += ((threadIdx.x & 63u) == (k)) ? now_ - ph_t0 : 0ull;      \
+    ph_t0 = now_;                                                      \
+  } while (0)
+#define CTCBEAM_PHASE_COUNT(k)                                 \
+  do {                                                         \
+    ph_acc += ((threadIdx.x & 63u) == (k)) ? 1ull : 0ull;      \
   } while (0)
 #else
 #define CTCBEAM_PHASE_MARK(k) \
   do {                        \
+  } while (0)
+#define CTCBEAM_PHASE_COUNT(k) \
+  do {                         \
   } while (0)
 #endif
 

@@ -8,7 +8,8 @@ counters at every phase boundary), then on a GPU:
     python -m paper_2508_07315_amd.phase_profile --config 3 --mode greedy
 
 Prints, per phase of the frame step (beam search: fill, barrier A,
-candidates, barrier B, filter, barrier C, rank, barrier D, update; greedy:
+candidates, barrier B, filter, barrier C, rank, barrier D, and the update
+as prune + recombination, new state, chunk plan and the rest; greedy:
 scoring, the wave's best, the exchange barrier, the decision, chain headers +
 fold, continuations, log-prob row loads), the mean cycles per frame of each
 wave, averaged over the utterances (weighted by their frames), and the mean
@@ -21,8 +22,13 @@ import math
 import os
 import sys
 
-PHASES = {"beam": ["fill", "bar A", "cand", "bar B", "filter", "bar C", "rank", "bar D", "update"],
-          "greedy": ["score", "best", "barrier", "decide", "hdr+fold", "arcs", "rows"]}
+# (counter word, name); the beam update is split into prune + recombination,
+# new state, chunk plan and the rest (one slot per lane; two slots per lane
+# count the whole update under "upd rest")
+PHASES = {"beam": [(0, "fill"), (1, "bar A"), (2, "cand"), (3, "bar B"), (4, "filter"), (5, "bar C"),
+                   (6, "rank"), (7, "bar D"), (11, "upd merge"), (12, "upd state"), (13, "upd plan"),
+                   (8, "upd rest")],
+          "greedy": list(enumerate(["score", "best", "barrier", "decide", "hdr+fold", "arcs", "rows"]))}
 WAVES = 8
 WORDS = 16
 
@@ -80,13 +86,13 @@ def main(argv=None):
     print(f"{w.name} {args.mode} K={1 if args.mode == 'greedy' else w.K} theta={theta}: {int(nf)} frames, "
           f"{chunks.sum() / max(nf, 1):.2f} {what}/frame")
     print("cycles per frame by wave (mean over utterances, weighted by frames)")
-    print("phase    " + " ".join(f"{'w%d' % q:>7s}" for q in range(WAVES)) + "     mean")
+    print("phase     " + " ".join(f"{'w%d' % q:>7s}" for q in range(WAVES)) + "     mean")
     tot = np.zeros(WAVES)
-    for k, name in enumerate(PHASES[args.mode]):
+    for k, name in PHASES[args.mode]:
         per = ph[:, :, k].sum(axis=0) / max(nf, 1)
         tot += per
-        print(f"{name:8s} " + " ".join(f"{v:7.0f}" for v in per) + f"  {per.mean():7.0f}")
-    print(f"{'total':8s} " + " ".join(f"{v:7.0f}" for v in tot) + f"  {tot.mean():7.0f}")
+        print(f"{name:9s} " + " ".join(f"{v:7.0f}" for v in per) + f"  {per.mean():7.0f}")
+    print(f"{'total':9s} " + " ".join(f"{v:7.0f}" for v in tot) + f"  {tot.mean():7.0f}")
 
 
 if __name__ == "__main__":
