@@ -167,7 +167,7 @@ __device__ __forceinline__ bool dup_by_sort(uint64_t key, int lane, uint32_t& lo
 // every frame (fill, barrier A, candidates, barrier B, filter, barrier C,
 // rank, barrier D, the update's remainder; then the frame and chunk counts;
 // then, one slot per lane, the update's prune + recombination, new state and
-// chunk plan) and writes them after the [B, 8] statistics as
+// chunk plan; then the bound, split from the filter) and writes them after the [B, 8] statistics as
 // [B, kWaves, kPhaseWords] int64.
 
 // SPL = beam slots per lane: slot j lives in lane j % 64, register set
@@ -1385,6 +1385,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         if constexpr (!kSmallK) tblank = blank_bound();
         // an infinite bound admits every finite candidate and no -inf one
         const float tau = fmaxf(fmaxf(fmaxf(tau_run, tc), tblank), -__FLT_MAX__);
+        CTCBEAM_PHASE_MARK(14);
         // most waves hold no survivor: their lane maxima say so
         if (__ballot(lmax >= tau) != 0ull) {  // uniform
           uint32_t qmask = 0u;

@@ -8,7 +8,7 @@ counters at every phase boundary), then on a GPU:
     python -m paper_2508_07315_amd.phase_profile --config 3 --mode greedy
 
 Prints, per phase of the frame step (beam search: fill, barrier A,
-candidates, barrier B, filter, barrier C, rank, barrier D, and the update
+candidates, barrier B, bound, filter, barrier C, rank, barrier D, and the update
 as prune + recombination, new state, chunk plan and the rest; greedy:
 scoring, the wave's best, the exchange barrier, the decision, chain headers +
 fold, continuations, log-prob row loads), the mean cycles per frame of each
@@ -25,7 +25,7 @@ import sys
 # (counter word, name); the beam update is split into prune + recombination,
 # new state, chunk plan and the rest (one slot per lane; two slots per lane
 # count the whole update under "upd rest")
-PHASES = {"beam": [(0, "fill"), (1, "bar A"), (2, "cand"), (3, "bar B"), (4, "filter"), (5, "bar C"),
+PHASES = {"beam": [(0, "fill"), (1, "bar A"), (2, "cand"), (3, "bar B"), (14, "bound"), (4, "filter"), (5, "bar C"),
                    (6, "rank"), (7, "bar D"), (11, "upd merge"), (12, "upd state"), (13, "upd plan"),
                    (8, "upd rest")],
           "greedy": list(enumerate(["score", "best", "barrier", "decide", "hdr+fold", "arcs", "rows"]))}
