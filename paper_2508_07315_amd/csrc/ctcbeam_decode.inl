@@ -797,6 +797,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
     }
     float tau_run = kNegInf;
     float gacc = kNegInf;  // top 64 group maxima of the frame's chunks so far (K > 8)
+    float gacc_hi = kNegInf;  // two slots per lane: positions 64..127 of the top 128
     int nfin = 0;
     // survivors carried in the pool from chunks whose rank was skipped
     int carry = 0;
@@ -1358,29 +1359,22 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           gacc = bitonic_merge<64, 64, 32>(fmaxf(SKIP ? gacc : kNegInf, v), lane);
           tc = rdlane(gacc, K - 1);
         } else {
-          // K-th largest of 128 maxima, two sorted halves a and b: the largest
-          // value x with at least K maxima >= x (counts by binary search)
-          const float a = wave_sort_desc<64>(s_top[lane], lane);
-          const float bb = wave_sort_desc<64>(s_top[64 + lane], lane);
-          const float a_last = rdlane(a, 63), b_last = rdlane(bb, 63);
-          auto count_ge = [&](float x) __attribute__((always_inline)) {
-            // #{a >= x}: 64 if the smallest is, else a search over counts 0..63
-            int pa = 0, pb = 0;
-#pragma unroll
-            for (int step = 32; step >= 1; step >>= 1) {
-              const float va = __int_as_float(__builtin_amdgcn_ds_bpermute((pa + step - 1) << 2, __float_as_int(a)));
-              const float vb = __int_as_float(__builtin_amdgcn_ds_bpermute((pb + step - 1) << 2, __float_as_int(bb)));
-              pa += (va >= x) ? step : 0;
-              pb += (vb >= x) ? step : 0;
-            }
-            return (a_last >= x ? 64 : pa) + (b_last >= x ? 64 : pb);
-          };
-          const float ca = count_ge(a) >= K ? a : kNegInf;
-          const float cb = count_ge(bb) >= K ? bb : kNegInf;
-          float v = fmax_sel(ca, cb);
-#pragma unroll
-          for (int d = 1; d < 64; d <<= 1) v = fmax_sel(v, xor_lane(v, d, lane));
-          tc = v;
+          // This chunk's 128 group maxima, sorted ascending, merged into the
+          // frame's running top 128 (descending; positions 0..63 in gacc, 64..127
+          // in gacc_hi), as for one slot per lane.  The ascending sort runs on
+          // the negated values: the halves sorted descending and ascending
+          // form a bitonic sequence, merged descending by one exchange
+          // between the halves and a 64-lane merge in each.
+          const float e0 = wave_sort_desc<64>(-s_top[lane], lane);
+          const float f1 = -wave_sort_desc<64>(s_top[64 + lane], lane);
+          const float n0 = -bitonic_merge<64, 64, 32>(fmaxf(e0, f1), lane);
+          const float n1 = -bitonic_merge<64, 64, 32>(fminf(e0, f1), lane);
+          // the elementwise maximum with the descending top 128 is bitonic and
+          // holds the top 128 of the union
+          const float m0 = fmaxf(gacc, n0), m1 = fmaxf(gacc_hi, n1);
+          gacc = bitonic_merge<64, 64, 32>(fmaxf(m0, m1), lane);
+          gacc_hi = bitonic_merge<64, 64, 32>(fminf(m0, m1), lane);
+          tc = K <= 64 ? rdlane(gacc, K - 1) : rdlane(gacc_hi, K - 65);
         }
         if constexpr (!kSmallK) tblank = blank_bound();
         // an infinite bound admits every finite candidate and no -inf one
@@ -1465,6 +1459,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         const uint32_t* prec = s_rec + rcur * (KMX * RW);
         uint32_t* nrec = s_rec + (rcur ^ 1) * (KMX * RW);
         if (!s_overflow) {
+          CTCBEAM_PHASE_COUNT(15);  // ranks
           const int n = min(s_nbuf, kCap);
           const int N = K + n;
           nfin = 0;
@@ -1500,6 +1495,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
               if (rep) s_rinc[Q][myrank] = (lane < K) ? s_rinc[P][lane] : s_pinc[lane - K];
             }
           } else if (kTreeRank && N > 192 && N <= kThreads) {
+            CTCBEAM_PHASE_COUNT(16);  // merge-tree ranks
             // K <= 64 of 193..512 entries (a few blocks of 64 are cheaper to
             // rank against each other): each wave sorts its 64 entries by
             // (score desc, index asc) as 64-bit keys, then a tree of pairwise
@@ -1569,6 +1565,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           } else {
             // blocks of 64 entries: this wave ranks entries qb + (wave + 8u)
             // against every entry, lane f holding entry fb + f
+            CTCBEAM_PHASE_COUNT(16);  // block ranks
             for (int qb = 0; qb < N; qb += 64) {
               const int q = qb + lane;
               uint4 eq = make_uint4(__float_as_uint(kNegInf), 0xFFFFFFFFu, 0u, 0u);
@@ -1625,6 +1622,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
             }
           }
         } else {
+          CTCBEAM_PHASE_COUNT(17);  // pool overflows (K-step extraction)
           // exact extraction over (reserved region P) U (pool entries carried
           // from earlier chunks) U (this chunk's candidates)
           uint64_t prev = ~0ull;

@@ -37,7 +37,7 @@ constexpr uint32_t kWsMagic = 0x42435443u;  // "CTCB"
 // previous mark to word k, CTCBEAM_PHASE_COUNT(k) adds one.  One register
 // pair per wave keeps the profiling build's register use close to the
 // product's.  Product builds compile none of it.
-constexpr int kPhaseWords = 16;
+constexpr int kPhaseWords = 20;
 #ifdef CTCBEAM_PHASE_CLOCKS
 #define CTCBEAM_PHASE_MARK(k)                                          \
   do {                                                                 \

@@ -30,7 +30,7 @@ PHASES = {"beam": [(0, "fill"), (1, "bar A"), (2, "cand"), (3, "bar B"), (14, "b
                    (8, "upd rest")],
           "greedy": list(enumerate(["score", "best", "barrier", "decide", "hdr+fold", "arcs", "rows"]))}
 WAVES = 8
-WORDS = 16
+WORDS = 20
 
 
 def main(argv=None):
@@ -93,6 +93,10 @@ def main(argv=None):
         tot += per
         print(f"{name:9s} " + " ".join(f"{v:7.0f}" for v in per) + f"  {per.mean():7.0f}")
     print(f"{'total':9s} " + " ".join(f"{v:7.0f}" for v in tot) + f"  {tot.mean():7.0f}")
+    if args.mode == "beam":
+        per = lambda k: ph[:, 0, k].sum() / max(nf, 1)
+        print(f"ranks per frame {per(15):.2f} (block or merge-tree ranks of more than 64 entries "
+              f"{per(16):.2f}), pool overflows per frame {per(17):.3f}")
 
 
 if __name__ == "__main__":
