@@ -1355,8 +1355,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
           // into the frame's running top 64 (descending): the elementwise
           // maximum of the two is bitonic and holds the top 64 of the union
           // (without rank skipping each chunk's rank sets tau_run instead)
-          const float v = -wave_sort_desc<64>(-s_top[lane], lane);
-          gacc = bitonic_merge<64, 64, 32>(fmaxf(SKIP ? gacc : kNegInf, v), lane);
+          // (a chunk none of whose maxima beats the K-th largest so far
+          // leaves the top K as it is: no sort)
+          const float kth = rdlane(gacc, K - 1);
+          if (!SKIP || __ballot(s_top[lane] > kth) != 0ull) {  // uniform
+            const float v = -wave_sort_desc<64>(-s_top[lane], lane);
+            gacc = bitonic_merge<64, 64, 32>(fmaxf(SKIP ? gacc : kNegInf, v), lane);
+          }
           tc = rdlane(gacc, K - 1);
         } else {
           // This chunk's 128 group maxima, sorted ascending, merged into the
