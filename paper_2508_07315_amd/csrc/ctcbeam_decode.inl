@@ -1079,7 +1079,7 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
         kslot[i] = static_cast<int>((CACHE || kGroups) ? (hz & 0xFFu) : hz);
         krow[i] = (CACHE || kGroups) ? ((hz >> 8) & 0xFFu) : static_cast<uint32_t>(i);
         kbrow[i] = kGroups ? ((hz >> 16) & 0xFFu) : static_cast<uint32_t>(i);
-        kpot[i] = static_cast<int>(h0.w);
+        kpot[i] = static_cast<int>(kGroups ? __builtin_amdgcn_readfirstlane(h0.w) : h0.w);
 #pragma unroll
         for (int l0 = 0; l0 < (kFoldRows ? 0 : NL); l0 += 4) {
           const uint4 h = *reinterpret_cast<const uint4*>(rr + 4 + l0);
@@ -1096,56 +1096,125 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       uint32_t lhi[kKeepLm ? NC : 1];
       float lmax = kNegInf;
       float rmax[KCR];  // per chunk row: maximum over this lane's labels
-#pragma unroll
-      for (int i = 0; i < KCR; ++i) {
+      if constexpr (kGroups) {
+        // Fill groups: the beams of an LM state are adjacent, so a row in the
+        // state of the row before reads the same LM terms, and a row with the
+        // same boosting row and pot the same boosting terms; they are kept
+        // from that row rather than read and folded again (uniform branches).
+        float avk[LPT], bvk[LPT];
+        uint32_t lhk[LPT];
 #pragma unroll
         for (int jj = 0; jj < LPT; ++jj) {
-          const int r = i * LPT + jj;
-          const int c = tid + jj * kThreads;
-          const uint32_t e = static_cast<uint32_t>(i * V) + rcc[jj];
-          // LM entry: the row this beam reads (shared with its state's first beam)
-          const uint32_t el = kGroups ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
-          const float x0 = ksc[i] + rD[jj];
-          float x1 = x0 + beta;
-          if (HAS_LM) {
-            if constexpr (CACHE) {
-              // a cached row holds every token: the fold or the arc, with
-              // the LM target state
-              const uint64_t ent = lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]];
-              x1 = x1 + __uint_as_float(static_cast<uint32_t>(ent));
-              lhi[r] = static_cast<uint32_t>(ent >> 32) & kTargetMask;
-            } else if constexpr (kFoldRows) {
-              // the chunk's rows hold every token: the fold (order 0, the
-              // token) or an explicit arc (its staging slot, resolved later)
-              const uint64_t ent = lmrow[el];
-              x1 = x1 + __uint_as_float(static_cast<uint32_t>(ent));
-              if constexpr (kKeepLm) lhi[r] = static_cast<uint32_t>(ent >> 32);
-            } else {
+          avk[jj] = 0.0f;
+          bvk[jj] = 0.0f;
+          lhk[jj] = 0u;
+        }
+#pragma unroll
+        for (int i = 0; i < KCR; ++i) {
+          const bool lm_new = i == 0 || krow[i] != krow[i > 0 ? i - 1 : 0];
+          const bool bt_new = i == 0 || kbrow[i] != kbrow[i > 0 ? i - 1 : 0] || kpot[i] != kpot[i > 0 ? i - 1 : 0];
+          if (HAS_LM && lm_new) {
+#pragma unroll
+            for (int jj = 0; jj < LPT; ++jj) {
+              // LM entry: the row this beam reads (its state's row in the group)
+              const uint32_t el = krow[i] * static_cast<uint32_t>(V) + rcc[jj];
               const uint64_t ent = lmrow[el];
               const uint32_t hi = static_cast<uint32_t>(ent >> 32);
-              float v = rP1[jj];
+              if constexpr (kFoldRows) {
+                // the chunk's rows hold every token: the fold (order 0, the
+                // token) or an explicit arc (its staging slot, resolved later)
+                avk[jj] = __uint_as_float(static_cast<uint32_t>(ent));
+                lhk[jj] = hi;
+              } else {
+                float v = rP1[jj];
 #pragma unroll
-              for (int l = 0; l < NL; ++l) v = v + kbo[i][l];
-              const bool has = hi >= genhi;
-              const float av = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
-              x1 = x1 + av;
-              // the LM target: an explicit arc's staging slot (resolved
-              // later), or the token's unigram state
-              if constexpr (kKeepLm) lhi[r] = has ? hi : rcc[jj];
+                for (int l = 0; l < NL; ++l) v = v + kbo[i][l];
+                const bool has = hi >= genhi;
+                avk[jj] = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
+                // the LM target: an explicit arc's staging slot (resolved
+                // later), or the token's unigram state
+                lhk[jj] = has ? hi : rcc[jj];
+              }
             }
           }
-          if (HAS_BT) {
-            const uint32_t be = btrow[kGroups ? kbrow[i] * static_cast<uint32_t>(V) + rcc[jj] : e];
-            const uint32_t bk = (be >= genhi) ? be : rRoot[jj];
-            const int pre = static_cast<int>((bk >> 20) & 63u);
-            const float bv = boost_w * static_cast<float>(pre - kpot[i]);
-            x1 = x1 + bv;
+          if (HAS_BT && bt_new) {
+#pragma unroll
+            for (int jj = 0; jj < LPT; ++jj) {
+              const uint32_t be = btrow[kbrow[i] * static_cast<uint32_t>(V) + rcc[jj]];
+              const uint32_t bk = (be >= genhi) ? be : rRoot[jj];
+              const int pre = static_cast<int>((bk >> 20) & 63u);
+              bvk[jj] = boost_w * static_cast<float>(pre - kpot[i]);
+            }
           }
-          const float x = (c != klast[i]) ? x1 : x0;
-          cand[r] = x;
-          rmax[i] = jj == 0 ? x : fmaxf(rmax[i], x);
+#pragma unroll
+          for (int jj = 0; jj < LPT; ++jj) {
+            const int r = i * LPT + jj;
+            const int c = tid + jj * kThreads;
+            const float x0 = ksc[i] + rD[jj];
+            float x1 = x0 + beta;
+            if (HAS_LM) {
+              x1 = x1 + avk[jj];
+              if constexpr (kKeepLm) lhi[r] = lhk[jj];
+            }
+            if (HAS_BT) x1 = x1 + bvk[jj];
+            const float x = (c != klast[i]) ? x1 : x0;
+            cand[r] = x;
+            rmax[i] = jj == 0 ? x : fmaxf(rmax[i], x);
+          }
+          lmax = fmaxf(lmax, rmax[i]);
         }
-        lmax = fmaxf(lmax, rmax[i]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < KCR; ++i) {
+#pragma unroll
+          for (int jj = 0; jj < LPT; ++jj) {
+            const int r = i * LPT + jj;
+            const int c = tid + jj * kThreads;
+            const uint32_t e = static_cast<uint32_t>(i * V) + rcc[jj];
+            // LM entry: the row this beam reads (shared with its state's first beam)
+            const uint32_t el = kGroups ? krow[i] * static_cast<uint32_t>(V) + rcc[jj] : e;
+            const float x0 = ksc[i] + rD[jj];
+            float x1 = x0 + beta;
+            if (HAS_LM) {
+              if constexpr (CACHE) {
+                // a cached row holds every token: the fold or the arc, with
+                // the LM target state
+                const uint64_t ent = lmrow[krow[i] * static_cast<uint32_t>(V) + rcc[jj]];
+                x1 = x1 + __uint_as_float(static_cast<uint32_t>(ent));
+                lhi[r] = static_cast<uint32_t>(ent >> 32) & kTargetMask;
+              } else if constexpr (kFoldRows) {
+                // the chunk's rows hold every token: the fold (order 0, the
+                // token) or an explicit arc (its staging slot, resolved later)
+                const uint64_t ent = lmrow[el];
+                x1 = x1 + __uint_as_float(static_cast<uint32_t>(ent));
+                if constexpr (kKeepLm) lhi[r] = static_cast<uint32_t>(ent >> 32);
+              } else {
+                const uint64_t ent = lmrow[el];
+                const uint32_t hi = static_cast<uint32_t>(ent >> 32);
+                float v = rP1[jj];
+#pragma unroll
+                for (int l = 0; l < NL; ++l) v = v + kbo[i][l];
+                const bool has = hi >= genhi;
+                const float av = has ? __uint_as_float(static_cast<uint32_t>(ent)) : alpha * v;
+                x1 = x1 + av;
+                // the LM target: an explicit arc's staging slot (resolved
+                // later), or the token's unigram state
+                if constexpr (kKeepLm) lhi[r] = has ? hi : rcc[jj];
+              }
+            }
+            if (HAS_BT) {
+              const uint32_t be = btrow[kGroups ? kbrow[i] * static_cast<uint32_t>(V) + rcc[jj] : e];
+              const uint32_t bk = (be >= genhi) ? be : rRoot[jj];
+              const int pre = static_cast<int>((bk >> 20) & 63u);
+              const float bv = boost_w * static_cast<float>(pre - kpot[i]);
+              x1 = x1 + bv;
+            }
+            const float x = (c != klast[i]) ? x1 : x0;
+            cand[r] = x;
+            rmax[i] = jj == 0 ? x : fmaxf(rmax[i], x);
+          }
+          lmax = fmaxf(lmax, rmax[i]);
+        }
       }
       if constexpr (rep) {
         // repeat-scoring variant: the repeat of a live row's last label (a
