@@ -7,9 +7,10 @@ so the results must equal the CPU oracle's (tokens bit-exact, scores within
 
 * 5- and 6-gram LMs of a few thousand n-grams (most hypotheses back off to
   short, shared states) with K = 9..128 (one and two beam slots per lane),
-  vocabularies of 300, 400, 1024 and 1500 tokens (one, two and four labels
-  per lane), with and without boosting, theta = inf and 12, 1-best and
-  N-best;
+  vocabularies of 300, 400, 1024, 1500 and 3000 tokens (one, two, four and
+  eight labels per lane), with and without boosting, theta = inf and 12,
+  1-best and N-best.  At 3000 tokens a group holds one boosting list, so an
+  LM state whose beams hold several lists is split over groups list by list;
 * log-sum-exp recombination and repeat scoring on the same path;
 * a witness that the final beams do share LM states (the longest suffix of
   <s> + tokens that is an n-gram of the model), so that shared rows are what
@@ -23,17 +24,20 @@ import pytest
 import oracle
 import paper_2508_07315_amd as P
 import workloads as W
-from gpu_helpers import compare, device, handles, log, oracle_threads
+from gpu_helpers import compare, device, handles, log, oracle_bt, oracle_lm, oracle_threads
 
 pytestmark = pytest.mark.gpu
 
 
 def _workload(order, V, K, boost, seed):
     counts = tuple([min(3 * V, (V + 1) ** 2)] + [2 * V] * (order - 2))
+    # above 2048 tokens a group holds one list: many Zipf phrases put the
+    # beams of one LM state in several boosting states
+    spec = W.BoostSpec(5000, 2, 4, "zipf", seed + 2) if V > 2048 else W.BoostSpec(300, 2, 5, "uniform", seed + 2)
     return W.CONFIGS[6].replace(
         B=3, T=90, V=V, K=K, lengths=("uniform", 40, 90), seed=seed,
         lm=W.LMSpec(order=order, counts=counts, seed=seed + 1),
-        boost=W.BoostSpec(300, 2, 5, "uniform", seed + 2) if boost else None,
+        boost=spec if boost else None,
         boost_w=1.5 if boost else 0.0)
 
 
@@ -70,7 +74,8 @@ def _lm_state(entries, order, bos, toks):
 @pytest.mark.parametrize("order,V,K,boost", [
     (5, 1024, 16, False), (5, 1024, 64, True), (6, 1024, 40, True), (6, 1024, 64, False),
     (6, 1024, 9, True), (6, 300, 33, True), (5, 1500, 64, False), (5, 1500, 24, True),
-    (6, 1024, 100, True), (5, 1024, 128, False), (6, 400, 77, True)])
+    (6, 1024, 100, True), (5, 1024, 128, False), (6, 400, 77, True),
+    (5, 3000, 24, True), (5, 3000, 64, True)])
 def test_shared_rows(order, V, K, boost):
     w = _workload(order, V, K, boost, 31000 + 97 * order + K)
     lm, bt, olm, obt = handles(w)
@@ -143,3 +148,44 @@ def test_final_beams_share_lm_states():
     r = oracle.decode(lp, lens, w.K, w.alpha, w.beta, 0.0, lm=olm, n_threads=oracle_threads(),
                       want_nbest=True)
     _compare_nbest(gn, r, what="witness workload")
+
+
+def test_wide_vocabulary_splits_states_over_groups():
+    # Witness for the (5, 3000, 64, boosting) case above: in some frames of
+    # the oracle's search the live beams of one LM state sit in two boosting
+    # states, more than a group holds at 3000 tokens (one list), so the plan
+    # splits that state over groups list by list.
+    import collections
+    order, V, K = 5, 3000, 64
+    w = _workload(order, V, K, True, 31000 + 97 * order + K)
+    olm, obt = oracle_lm(w.lm, w.V), oracle_bt(w.boost, w.V)
+    lp = W.make_logprobs(w)
+    lens = W.make_lengths(w)
+    r = oracle.decode(lp, lens, K, w.alpha, w.beta, w.boost_w, lm=olm, bt=obt,
+                      n_threads=oracle_threads(), want_trace=True)
+    arrays = W.lm_for(w.lm, w.V)
+    entries = [set(map(tuple, ids.tolist())) for ids in arrays["ids"][: order - 1]]
+    bp, ss, Wd = r["bp_index"], r["slot_scores"], V + 1
+    split = 0
+    for b in range(w.B):
+        ys = [[] for _ in range(K)]
+        last = [V] * K
+        for t in range(int(lens[b])):
+            nys, nlast = [], []
+            for j in range(K):
+                p, c = divmod(int(bp[b, t, j]), Wd)
+                y = list(ys[p])
+                if c != V and c != last[p]:
+                    y.append(c)
+                nys.append(y)
+                nlast.append(c)
+            ys, last = nys, nlast
+            by_state = collections.defaultdict(set)
+            for j in range(K):
+                if np.isfinite(ss[b, t, j]):
+                    q = tuple(obt.run(ys[j])[1])
+                    if q:
+                        by_state[_lm_state(entries, order, V + 1, ys[j])].add(q)
+            split += any(len(v) >= 2 for v in by_state.values())
+    log(f"frames with an LM state in two boosting states: {split}")
+    assert split > 0
