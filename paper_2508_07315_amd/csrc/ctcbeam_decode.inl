@@ -1518,11 +1518,13 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
       // The best K go to region Q in rank order; after the last chunk the
       // winners' successor records go to s_rec[rcur ^ 1] instead.  Before
       // the last chunk the rank runs only when the pool is more than half
-      // full (or overflowed): otherwise the survivors stay in the pool for
-      // the next chunk (with large beams most chunks skip it).
+      // full (a quarter with two slots per lane, whose block rank costs the
+      // square of the pool; an earlier rank also tightens the bound) or
+      // overflowed: otherwise the survivors stay in the pool for the next
+      // chunk (with large beams most chunks skip it).
       const bool last_chunk = ch + 1 == nch;
       const int npool = s_nbuf;
-      if (SKIP && !last_chunk && !s_overflow && npool <= kCap / 2) {  // uniform
+      if (SKIP && !last_chunk && !s_overflow && npool <= (SPL > 1 ? kCap / 4 : kCap / 2)) {  // uniform
         carry = npool;
         cs += kc;
         CTCBEAM_PHASE_COUNT(10);  // chunks
