@@ -219,10 +219,10 @@ __global__ void __launch_bounds__(kThreads) decode_kernel(KernelParams p) {
   // slots per lane, fold in the scoring: cheaper than the extra LDS maxima.
   constexpr bool kFoldRows = CACHE || (NL >= 4 && SPL == 1);
   // Fill groups (beams over one chunk, no row cache): the update orders the
-  // live beams by LM state and, within a state, by boosting list, and cuts
-  // that order into groups of consecutive chunks whose distinct LM states
-  // (at most KSEG), boosting lists (at most KCR - 1) and staged arcs (at
-  // most kLmStage) fit the rows.  A state or list has one row per group,
+  // live beams by LM state and cuts that order into groups of consecutive
+  // chunks whose distinct LM states (at most KSEG), boosting lists (at most
+  // KCR - 1) and staged arcs (at most kLmStage) fit the rows (a state whose
+  // own lists exceed a group is split by list).  A state or list has one row per group,
   // filled at the group's first chunk; the group's other chunks skip the
   // fill and its barrier.  Large beams hold few distinct states and lists
   // (at K = 64 about 10 and 6), so a frame fills about two groups.
